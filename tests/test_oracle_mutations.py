@@ -1,0 +1,86 @@
+"""The oracle's pins must fail when a plausible mistake is planted in the oracle.
+
+Each case patches one oracle function with a wrong variant (a dropped factor, a wrong
+index, a non-exact solver) and checks that the pin meant to guard it now fails.
+"""
+import numpy as np
+import pytest
+
+from oracle import affinity as orc
+from oracle import layout as lay
+from tests import test_oracle_affinity as pa
+from tests import test_oracle_layout as pl
+
+
+@pytest.fixture(scope="module")
+def tiny():
+    return pa._data()
+
+
+def test_wrong_silu_derivative_is_caught(tiny, monkeypatch):
+    def bad(g):
+        s = orc.sigmoid(g)
+        return s * (1.0 + g * s)
+    monkeypatch.setattr(orc, "silu_prime", bad)
+    with pytest.raises(AssertionError):
+        pa.test_damage_equals_autograd_jvp(tiny)
+
+
+def test_dropped_gain_in_head_piece_is_caught(tiny, monkeypatch):
+    orig = orc.head_pieces
+
+    def bad(x, attn, w_o, gamma, eps):
+        return orig(x, attn, w_o, np.ones_like(gamma), eps)
+    monkeypatch.setattr(orc, "head_pieces", bad)
+    with pytest.raises(AssertionError):
+        pa.test_damage_equals_autograd_jvp(tiny)
+
+
+def test_wrong_group_mapping_is_caught(tiny, monkeypatch):
+    monkeypatch.setattr(orc, "group_of_head", lambda H, G: np.arange(H) % G)
+    with pytest.raises(AssertionError):
+        pa.test_single_head_affinity_equals_jvp_square_sum(tiny)
+
+
+def test_unsquared_down_norm_is_caught(tiny, monkeypatch):
+    orig = orc._aggregate
+
+    def bad(s, w_down, G):
+        return orig(s, np.sqrt(np.abs(w_down)) * np.sign(w_down), G)   # ||w||, not ||w||^2
+    monkeypatch.setattr(orc, "_aggregate", bad)
+    with pytest.raises(AssertionError):
+        pa.test_down_column_scale(tiny)
+
+
+def test_mean_instead_of_token_sum_is_caught(tiny, monkeypatch):
+    orig = orc.affinity_literal
+
+    def bad(x, attn, *a, **k):
+        return orig(x, attn, *a, **k) / x.shape[0]
+    monkeypatch.setattr(orc, "affinity_literal", bad)
+    with pytest.raises(AssertionError):
+        pa.test_token_chunks_add(tiny)
+
+
+def test_heuristic_assignment_is_caught(monkeypatch):
+    def greedy(M):
+        I, L = M.shape
+        nu = np.empty(I, dtype=np.int64)
+        cap = [I // L] * L
+        for k in range(I):
+            for l in np.argsort(-M[k], kind="stable"):
+                if cap[l]:
+                    nu[k] = l
+                    cap[l] -= 1
+                    break
+        return nu
+    monkeypatch.setattr(lay, "optimal_assignment", greedy)
+    with pytest.raises(AssertionError):
+        for I, L, seed in [(8, 2, 1), (8, 4, 2), (9, 3, 4)]:
+            pl.test_assign_brute_force(I, L, seed)
+
+
+def test_wrong_tie_break_is_caught(monkeypatch):
+    monkeypatch.setattr(lay, "best_partition", lambda s, minimise=False: int(np.argmax(s[::-1]) * -1 + len(s) - 1))
+    with pytest.raises(AssertionError):
+        pl.test_head_step_brute_force_and_ties()
