@@ -1,0 +1,192 @@
+/*
+ * dtp.h - C ABI of libdtp.so: the data-parallel hot path of affinity-aware sharding for
+ * Delayed Tensor Parallelism (arXiv 2609.13846), for AMD Instinct MI355X (gfx950).
+ *
+ * The paper (Section 3) measures, over calibration tokens, how much each FFN neuron of a
+ * layer depends on each KV group of the same layer (the "up" affinity S_up[g, k]), then
+ * chooses balanced assignments of KV groups (h_i) and neurons (nu_i) to L devices that
+ * maximise the total co-located normalised affinity J (eq. "objective") by coordinate
+ * ascent: an exact balanced assignment of the neurons given the heads, and an exhaustive
+ * scan of the labelled balanced partitions of the KV groups given the neurons.
+ *
+ * Conventions shared by every entry point:
+ *   - Every function returns a dtp_status; nothing throws across the ABI.  On failure,
+ *     dtp_last_error() gives a thread-local message.
+ *   - Arguments are validated on the host before any GPU work is enqueued.
+ *   - "dev" pointers are device memory of the current HIP device; "host" pointers are
+ *     ordinary host memory.  The caller owns every buffer it passes; the library keeps
+ *     no caller pointer after a call returns.  Device tensors are dense row-major.
+ *   - `stream` is a hipStream_t (NULL = the default stream).  GPU work is enqueued on it
+ *     asynchronously; functions that return host results synchronise that stream first.
+ *   - Weights use the PyTorch nn.Linear layout [out_features, in_features].
+ *   - bf16 tensors are IEEE bfloat16 bit patterns (uint16); f32 tensors are float.
+ */
+#ifndef DTP_H
+#define DTP_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  DTP_OK = 0,
+  DTP_ERR_INVALID_ARG = -1,  /* null pointer, bad size, shape constraint violated */
+  DTP_ERR_UNSUPPORTED = -2,  /* a valid request outside what this build implements */
+  DTP_ERR_DEGENERATE = -3,   /* affinity all zero, negative or non-finite */
+  DTP_ERR_NO_MEMORY = -4,    /* host or device allocation failed */
+  DTP_ERR_HIP = -5           /* a HIP runtime call failed (message has the HIP string) */
+} dtp_status;
+
+typedef enum { DTP_BF16 = 0, DTP_F32 = 1 } dtp_dtype;
+
+/* Shapes of one decoder layer.  Query head h belongs to KV group h / (H/G).
+ * Constraints: all sizes > 0; H % G == 0; G <= 32; head_dim % 16 == 0; d_model % 8 == 0;
+ * rms_eps >= 0; dtype is DTP_BF16 (MFMA path) or DTP_F32 (reference-precision path). */
+typedef struct {
+  int32_t d_model;      /* d */
+  int32_t n_neurons;    /* I, SwiGLU FFN width */
+  int32_t n_q_heads;    /* H */
+  int32_t n_kv_groups;  /* G */
+  int32_t head_dim;     /* dh */
+  float rms_eps;        /* epsilon inside the FFN pre-norm: r = sqrt(mean(x^2) + eps) */
+  int32_t dtype;        /* dtp_dtype of every weight and activation */
+} dtp_layer_desc;
+
+typedef struct dtp_layer_s* dtp_layer;  /* opaque: folded weights and workspace of one layer */
+
+/* Allocate the device state of one layer (no weights yet).  *out receives the handle. */
+dtp_status dtp_layer_create(const dtp_layer_desc* desc, dtp_layer* out);
+
+/* Free a layer and everything it allocated.  NULL is accepted. */
+dtp_status dtp_layer_destroy(dtp_layer layer);
+
+/* Load and fold the weights of a layer (Section 3, "Affinity scores": p_h . w_k is
+ * re-associated as a_h . (W_o^(h) diag(gamma) w_k) / r, so each head's contraction runs
+ * over head_dim instead of d_model).  All pointers are dev, in the layer's dtype:
+ *   w_o    [d, H*dh]  attention output projection (o_proj.weight)
+ *   gamma  [d]        gain of the FFN pre-norm
+ *   w_gate [I, d], w_up [I, d]   SwiGLU gate and up projections
+ *   w_down [d, I]     down projection (its column k is w^d_k)
+ * Work is enqueued on `stream`; the inputs may be freed once the stream has passed it. */
+dtp_status dtp_layer_set_weights(dtp_layer layer, const void* w_o, const void* gamma,
+                                 const void* w_gate, const void* w_up, const void* w_down,
+                                 void* stream);
+
+/* Accumulate the raw first-order up affinity of n_tokens calibration tokens (Section 3,
+ * "Affinity scores", score FO):
+ *   A[g, k] += ||w^d_k||^2 * sum_t sum_{h in g} Delta_hk(t)^2,
+ *   Delta_hk = silu'(g_k) u_k (p_h . w^g_k) + silu(g_k) (p_h . w^u_k),
+ *   p_h = gamma * (a_h W_o^(h)) / r,  r = sqrt(mean(x^2) + eps),
+ * with g_k, u_k, r taken at the unmodified x (the rms change is ignored).  The mean over
+ * tokens of the paper is left to the caller (it cancels in the unit-mass normalisation).
+ *   x    dev [n_tokens, d]       residual entering the FFN pre-norm (layer dtype)
+ *   attn dev [n_tokens, H, dh]   per-head attention outputs a_h (layer dtype)
+ *   A    dev [G, I] float        accumulated in place (+=); deterministic for fixed shapes
+ * n_tokens == 0 is a no-op.  Requires dtp_layer_set_weights on an earlier call. */
+dtp_status dtp_affinity_accumulate(dtp_layer layer, const void* x, const void* attn,
+                                   int64_t n_tokens, float* A, void* stream);
+
+/* Timing of the affinity kernel with HIP events on the launch stream.  After
+ * dtp_layer_profile(layer, 1), every accumulate call records an event pair around each
+ * launch of its dominant kernel; dtp_layer_profile_read synchronises those events and
+ * returns the summed duration in milliseconds and the number of launches, then clears
+ * them.  dtp_layer_profile(layer, 0) stops recording. */
+dtp_status dtp_layer_profile(dtp_layer layer, int32_t enable);
+dtp_status dtp_layer_profile_read(dtp_layer layer, double* total_ms, int64_t* launches);
+
+/* ---------------------------------------------------------------------------------------
+ * Layout optimiser (Section 3, "Objective" and "Optimiser").
+ *
+ * Each raw affinity matrix is normalised to unit mass in exact fixed point:
+ *   E = floor(log2 max A); q_i = floor(A_i * 2^(40-E)); Q_i = floor(q_i * 2^48 / sum q).
+ * Codes are int64 and sum to 2^48 minus at most one unit per entry; J = J_int / 2^48,
+ * where J_int sums the codes of co-located (group, neuron) pairs.
+ * Ties: the best head partition is the one of lowest lexicographic rank; the neuron
+ * assignment is the lexicographically smallest optimal one.
+ * ------------------------------------------------------------------------------------- */
+
+/* Number of labelled balanced partitions of G groups over L devices, G!/((G/L)!)^L,
+ * or -1 when G % L != 0, L < 1 or G > 64. */
+int64_t dtp_partition_count(int32_t G, int32_t L);
+
+/* The partition of lexicographic rank `rank` (rank 0 is the contiguous h(g) = g/(G/L)).
+ * h: host [G] receives device indices. */
+dtp_status dtp_partition_unrank(int32_t G, int32_t L, int64_t rank, int32_t* h);
+
+/* Unit-mass fixed-point code of a raw affinity matrix.  A, Q: host [n], 1 <= n <= 2^20.
+ * DTP_ERR_DEGENERATE if any entry is negative or non-finite, or all are zero. */
+dtp_status dtp_encode_affinity(const float* A, int64_t n, int64_t* Q);
+
+/* Head step of one layer i (Section 3, "Optimiser"): score every labelled balanced
+ * partition h of the G KV groups,
+ *   score(h) = sum_g C[g, h(g)],
+ *   C[g, l]  = sum_{k: nu(k)=l} Q_up[g, k] + sum_{k: nu_prev(k)=l} Q_down_prev[k, g],
+ * on the GPU, one wavefront per partition.
+ *   Q_up        dev [G, I] int64    codes of layer i's up affinity
+ *   nu          dev [I] int32       neuron assignment of layer i (values in [0, L))
+ *   Q_down_prev dev [I, G] int64    codes of layer i-1's down affinity, or NULL
+ *   nu_prev     dev [I] int32       neuron assignment of layer i-1 (NULL iff Q_down_prev is)
+ *   minimise    0: best = highest score; 1: lowest
+ *   scores      dev [P] int64       score of every partition, by rank (P = partition count)
+ *   best_rank   host                rank of the best partition (lowest rank on ties)
+ * Requires G % L == 0, I % L == 0, G <= 64, P <= 2^24.  Synchronises `stream`. */
+dtp_status dtp_partition_scores(int32_t G, int32_t I, int32_t L, const int64_t* Q_up,
+                                const int32_t* nu, const int64_t* Q_down_prev,
+                                const int32_t* nu_prev, int32_t minimise, int64_t* scores,
+                                int64_t* best_rank, void* stream);
+
+/* Neuron step of one layer i (Section 3, "Optimiser"): the balanced nu maximising
+ * sum_k M[k, nu(k)] with I/L neurons per device, where
+ *   M[k, l] = sum_{g: h(g)=l} Q_up[g, k] + sum_{g: h_next(g)=l} Q_down[k, g].
+ * Exact (an optimal solution of the linear assignment with I/L slots per device), then
+ * the lexicographically smallest among all optimal ones.  Runs on the host.
+ *   Q_up   host [G, I] int64;  h host [G] int32 (balanced)
+ *   Q_down host [I, G] int64 or NULL;  h_next host [G] int32 (NULL iff Q_down is)
+ *   minimise  0: maximise; 1: minimise
+ *   nu     host [I] int32 output;  value host int64 output (sum_k M[k, nu(k)])
+ * Requires G % L == 0, I % L == 0, 1 <= L <= 8, G <= 64, I <= 2^24. */
+dtp_status dtp_balanced_assign(int32_t G, int32_t I, int32_t L, const int64_t* Q_up,
+                               const int32_t* h, const int64_t* Q_down, const int32_t* h_next,
+                               int32_t minimise, int32_t* nu, int64_t* value);
+
+/* Options of the coordinate ascent; NULL means the defaults
+ * {max_sweeps = 64, freeze_heads = 0, freeze_neurons = 0, minimise = 0, layer_mask = NULL}.
+ * freeze_*: keep that block at its contiguous start.  layer_mask (host [N] or NULL): a zero
+ * entry keeps layer i contiguous.  minimise: minimise J instead (anti-optimised layouts). */
+typedef struct {
+  int32_t max_sweeps;
+  int32_t freeze_heads;
+  int32_t freeze_neurons;
+  int32_t minimise;
+  const uint8_t* layer_mask;
+} dtp_ca_options;
+
+/* Coordinate ascent over a chain of N layers (Section 3, "Optimiser"): start from the
+ * contiguous head assignment h_i(g) = g/(G/L); each sweep runs the neuron step of every
+ * layer (host) and then the head step of every layer (GPU partition scores); stop at the
+ * first sweep whose J_int is not strictly better than the previous sweep's, or after
+ * max_sweeps.  Each matrix is encoded to unit mass separately.
+ *   A_up   dev [N, G, I] float  raw up affinity of each layer (from dtp_affinity_accumulate)
+ *   A_down dev [N-1, I, G] float raw down affinity, or NULL (then the layers decouple)
+ *   h      host [N, G] int32 output;  nu host [N, I] int32 output
+ *   J_fixed host int64 output (J_int);  J host double output (J_int / 2^48)
+ *   sweeps  host int32 output (sweeps run)
+ * Synchronises `stream`.  DTP_ERR_DEGENERATE if any matrix is all zero or not finite. */
+dtp_status dtp_coordinate_ascent(int32_t N, int32_t G, int32_t I, int32_t L,
+                                 const float* A_up, const float* A_down,
+                                 const dtp_ca_options* options, int32_t* h, int32_t* nu,
+                                 int64_t* J_fixed, double* J, int32_t* sweeps, void* stream);
+
+/* Human-readable name of a status code (static storage). */
+const char* dtp_status_string(dtp_status status);
+
+/* Detail of the last failure on the calling thread ("" if none). */
+const char* dtp_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* DTP_H */

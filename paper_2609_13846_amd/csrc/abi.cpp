@@ -1,0 +1,346 @@
+// C ABI of the layout side of libdtp.so: status strings, error reporting, validation,
+// the encoder, partition enumeration, the neuron step and the coordinate-ascent driver
+// (Section 3, "Objective" and "Optimiser").  The affinity entry points live in
+// affinity.hip.
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <thread>
+
+#include "dtp_internal.h"
+
+namespace dtp {
+
+namespace {
+thread_local char g_last_error[1024] = "";
+}
+
+dtp_status fail(dtp_status s, const char* fmt, ...) {
+  va_list ap;
+  va_start(ap, fmt);
+  std::vsnprintf(g_last_error, sizeof(g_last_error), fmt, ap);
+  va_end(ap);
+  return s;
+}
+
+void clear_error() { g_last_error[0] = '\0'; }
+
+namespace {
+
+// M[k][l] = sum_{g: h(g)=l} Q_up[g][k] + sum_{g: h_next(g)=l} Q_down[k][g], negated when
+// minimising (the solver maximises).
+void neuron_gain(int G, int I, int L, const int64_t* Q_up, const int32_t* h,
+                 const int64_t* Q_down, const int32_t* h_next, bool minimise,
+                 std::vector<int64_t>* M) {
+  M->assign((size_t)I * L, 0);
+  for (int g = 0; g < G; ++g) {
+    const int l = h[g];
+    const int64_t* q = Q_up + (size_t)g * I;
+    for (int k = 0; k < I; ++k) (*M)[(size_t)k * L + l] += q[k];
+  }
+  if (Q_down) {
+    for (int k = 0; k < I; ++k) {
+      const int64_t* q = Q_down + (size_t)k * G;
+      for (int g = 0; g < G; ++g) (*M)[(size_t)k * L + h_next[g]] += q[g];
+    }
+  }
+  if (minimise)
+    for (auto& v : *M) v = -v;
+}
+
+dtp_status check_balanced(const int32_t* h, int G, int L, const char* what) {
+  int count[kMaxGroups] = {0};
+  for (int g = 0; g < G; ++g) {
+    DTP_CHECK(h[g] >= 0 && h[g] < L, DTP_ERR_INVALID_ARG, "%s[%d] = %d is not a device in [0, %d)",
+              what, g, h[g], L);
+    ++count[h[g]];
+  }
+  for (int l = 0; l < L; ++l)
+    DTP_CHECK(count[l] == G / L, DTP_ERR_INVALID_ARG,
+              "%s is not balanced: device %d holds %d groups, expected %d", what, l, count[l],
+              G / L);
+  return DTP_OK;
+}
+
+dtp_status check_layout_sizes(int G, int I, int L, int max_devices) {
+  DTP_CHECK(G > 0 && I > 0 && L > 0, DTP_ERR_INVALID_ARG, "G=%d, I=%d, L=%d must be positive", G,
+            I, L);
+  DTP_CHECK(G % L == 0, DTP_ERR_INVALID_ARG, "G=%d is not a multiple of L=%d", G, L);
+  DTP_CHECK(I % L == 0, DTP_ERR_INVALID_ARG, "I=%d is not a multiple of L=%d", I, L);
+  DTP_CHECK(G <= kMaxGroups, DTP_ERR_UNSUPPORTED, "G=%d exceeds %d", G, kMaxGroups);
+  DTP_CHECK(L <= max_devices, DTP_ERR_UNSUPPORTED, "L=%d exceeds %d", L, max_devices);
+  DTP_CHECK(I <= (1 << 24), DTP_ERR_UNSUPPORTED, "I=%d exceeds 2^24", I);
+  return DTP_OK;
+}
+
+int64_t objective_int(int N, int G, int I, const std::vector<int64_t>& Qu,
+                      const std::vector<int64_t>& Qd, bool has_down,
+                      const std::vector<int32_t>& h, const std::vector<int32_t>& nu) {
+  int64_t J = 0;
+  for (int i = 0; i < N; ++i) {
+    const int64_t* q = Qu.data() + (size_t)i * G * I;
+    const int32_t* hi = h.data() + (size_t)i * G;
+    const int32_t* ni = nu.data() + (size_t)i * I;
+    for (int g = 0; g < G; ++g)
+      for (int k = 0; k < I; ++k)
+        if (hi[g] == ni[k]) J += q[(size_t)g * I + k];
+    if (has_down && i + 1 < N) {
+      const int64_t* qd = Qd.data() + (size_t)i * I * G;
+      const int32_t* hn = h.data() + (size_t)(i + 1) * G;
+      for (int k = 0; k < I; ++k)
+        for (int g = 0; g < G; ++g)
+          if (ni[k] == hn[g]) J += qd[(size_t)k * G + g];
+    }
+  }
+  return J;
+}
+
+struct DevBuf {
+  void* p = nullptr;
+  ~DevBuf() {
+    if (p) (void)hipFree(p);
+  }
+};
+
+}  // namespace
+}  // namespace dtp
+
+using namespace dtp;
+
+extern "C" {
+
+const char* dtp_status_string(dtp_status s) {
+  switch (s) {
+    case DTP_OK: return "DTP_OK";
+    case DTP_ERR_INVALID_ARG: return "DTP_ERR_INVALID_ARG";
+    case DTP_ERR_UNSUPPORTED: return "DTP_ERR_UNSUPPORTED";
+    case DTP_ERR_DEGENERATE: return "DTP_ERR_DEGENERATE";
+    case DTP_ERR_NO_MEMORY: return "DTP_ERR_NO_MEMORY";
+    case DTP_ERR_HIP: return "DTP_ERR_HIP";
+  }
+  return "DTP_ERR_UNKNOWN";
+}
+
+const char* dtp_last_error(void) { return g_last_error; }
+
+int64_t dtp_partition_count(int32_t G, int32_t L) { return count_partitions(G, L); }
+
+dtp_status dtp_partition_unrank(int32_t G, int32_t L, int64_t rank, int32_t* h) {
+  clear_error();
+  DTP_CHECK(h != nullptr, DTP_ERR_INVALID_ARG, "h is NULL");
+  const int64_t P = count_partitions(G, L);
+  DTP_CHECK(P > 0, DTP_ERR_INVALID_ARG, "no balanced partitions for G=%d, L=%d", G, L);
+  DTP_CHECK(rank >= 0 && rank < P, DTP_ERR_INVALID_ARG, "rank %lld outside [0, %lld)",
+            (long long)rank, (long long)P);
+  unrank_partition(G, L, rank, h);
+  return DTP_OK;
+}
+
+dtp_status dtp_encode_affinity(const float* A, int64_t n, int64_t* Q) {
+  clear_error();
+  DTP_CHECK(A != nullptr && Q != nullptr, DTP_ERR_INVALID_ARG, "A or Q is NULL");
+  DTP_CHECK(n >= 1 && n <= (int64_t(1) << 20), DTP_ERR_INVALID_ARG,
+            "n=%lld outside [1, 2^20]", (long long)n);
+  return encode_unit_mass(A, n, Q);
+}
+
+dtp_status dtp_balanced_assign(int32_t G, int32_t I, int32_t L, const int64_t* Q_up,
+                               const int32_t* h, const int64_t* Q_down, const int32_t* h_next,
+                               int32_t minimise, int32_t* nu, int64_t* value) {
+  clear_error();
+  dtp_status st = check_layout_sizes(G, I, L, kMaxAssignDevices);
+  if (st != DTP_OK) return st;
+  DTP_CHECK(Q_up && h && nu && value, DTP_ERR_INVALID_ARG, "a required pointer is NULL");
+  DTP_CHECK((Q_down == nullptr) == (h_next == nullptr), DTP_ERR_INVALID_ARG,
+            "Q_down and h_next must both be given or both be NULL");
+  if ((st = check_balanced(h, G, L, "h")) != DTP_OK) return st;
+  if (h_next && (st = check_balanced(h_next, G, L, "h_next")) != DTP_OK) return st;
+  std::vector<int64_t> M;
+  neuron_gain(G, I, L, Q_up, h, Q_down, h_next, minimise != 0, &M);
+  int64_t v = 0;
+  balanced_assign_exact(I, L, M.data(), nu, &v);
+  *value = minimise ? -v : v;
+  return DTP_OK;
+}
+
+dtp_status dtp_partition_scores(int32_t G, int32_t I, int32_t L, const int64_t* Q_up,
+                                const int32_t* nu, const int64_t* Q_down_prev,
+                                const int32_t* nu_prev, int32_t minimise, int64_t* scores,
+                                int64_t* best_rank, void* stream) {
+  clear_error();
+  dtp_status st = check_layout_sizes(G, I, L, 64);
+  if (st != DTP_OK) return st;
+  DTP_CHECK(Q_up && nu && scores && best_rank, DTP_ERR_INVALID_ARG, "a required pointer is NULL");
+  DTP_CHECK((Q_down_prev == nullptr) == (nu_prev == nullptr), DTP_ERR_INVALID_ARG,
+            "Q_down_prev and nu_prev must both be given or both be NULL");
+  const int64_t P = count_partitions(G, L);
+  DTP_CHECK(P > 0 && P <= kMaxPartitions, DTP_ERR_UNSUPPORTED,
+            "%lld partitions exceed the limit of %lld", (long long)P, (long long)kMaxPartitions);
+  hipStream_t s = (hipStream_t)stream;
+  // A two-layer view: layer 0 is empty padding so that layer 1 reads Q_down_prev / nu_prev
+  // as its incoming down edge.  Without a down edge one layer suffices.
+  const bool down = Q_down_prev != nullptr;
+  ScoreWorkspace ws;
+  st = score_workspace_create(&ws, down ? 2 : 1, G, I, L);
+  if (st != DTP_OK) {
+    score_workspace_destroy(&ws);
+    return st;
+  }
+  DevBuf qbuf, nbuf;
+  const int64_t* qu = Q_up;
+  const int32_t* nl = nu;
+  if (down) {
+    // layer 0 gets zero codes; layer 1 is the real layer
+    const size_t qbytes = sizeof(int64_t) * (size_t)G * I;
+    const size_t nbytes = sizeof(int32_t) * (size_t)I;
+    hipError_t e = hipMalloc(&qbuf.p, 2 * qbytes);
+    if (e == hipSuccess) e = hipMalloc(&nbuf.p, 2 * nbytes);
+    if (e == hipSuccess) e = hipMemsetAsync(qbuf.p, 0, qbytes, s);
+    if (e == hipSuccess)
+      e = hipMemcpyAsync((char*)qbuf.p + qbytes, Q_up, qbytes, hipMemcpyDeviceToDevice, s);
+    if (e == hipSuccess) e = hipMemcpyAsync(nbuf.p, nu_prev, nbytes, hipMemcpyDeviceToDevice, s);
+    if (e == hipSuccess)
+      e = hipMemcpyAsync((char*)nbuf.p + nbytes, nu, nbytes, hipMemcpyDeviceToDevice, s);
+    if (e != hipSuccess) {
+      score_workspace_destroy(&ws);
+      return fail(DTP_ERR_HIP, "staging the two-layer view failed: %s", hipGetErrorString(e));
+    }
+    qu = (const int64_t*)qbuf.p;
+    nl = (const int32_t*)nbuf.p;
+  }
+  st = launch_partition_scores(ws, qu, nl, Q_down_prev, nl, minimise, s);
+  if (st == DTP_OK) {
+    const int layer = down ? 1 : 0;
+    hipError_t e = hipMemcpyAsync(scores, ws.scores + (size_t)layer * P, sizeof(int64_t) * P,
+                                  hipMemcpyDeviceToDevice, s);
+    if (e == hipSuccess)
+      e = hipMemcpyAsync(best_rank, ws.best + layer, sizeof(int64_t), hipMemcpyDeviceToHost, s);
+    if (e == hipSuccess) e = hipStreamSynchronize(s);
+    if (e != hipSuccess) st = fail(DTP_ERR_HIP, "partition scoring failed: %s", hipGetErrorString(e));
+  }
+  score_workspace_destroy(&ws);
+  return st;
+}
+
+dtp_status dtp_coordinate_ascent(int32_t N, int32_t G, int32_t I, int32_t L, const float* A_up,
+                                 const float* A_down, const dtp_ca_options* options, int32_t* h,
+                                 int32_t* nu, int64_t* J_fixed, double* J, int32_t* sweeps,
+                                 void* stream) {
+  clear_error();
+  DTP_CHECK(N >= 1, DTP_ERR_INVALID_ARG, "N=%d must be >= 1", N);
+  dtp_status st = check_layout_sizes(G, I, L, kMaxAssignDevices);
+  if (st != DTP_OK) return st;
+  DTP_CHECK(A_up && h && nu && J_fixed && J && sweeps, DTP_ERR_INVALID_ARG,
+            "a required pointer is NULL");
+  DTP_CHECK(A_down == nullptr || N >= 2, DTP_ERR_INVALID_ARG, "A_down needs N >= 2");
+  dtp_ca_options opt = {64, 0, 0, 0, nullptr};
+  if (options) opt = *options;
+  DTP_CHECK(opt.max_sweeps >= 1, DTP_ERR_INVALID_ARG, "max_sweeps=%d must be >= 1",
+            opt.max_sweeps);
+  const int64_t P = count_partitions(G, L);
+  DTP_CHECK(P > 0 && P <= kMaxPartitions, DTP_ERR_UNSUPPORTED, "too many partitions (%lld)",
+            (long long)P);
+  hipStream_t s = (hipStream_t)stream;
+  const bool has_down = A_down != nullptr;
+  const size_t nup = (size_t)N * G * I, ndown = has_down ? (size_t)(N - 1) * I * G : 0;
+
+  // Raw affinity to the host, one unit-mass code per matrix.
+  std::vector<float> Au(nup), Ad(ndown);
+  DTP_HIP(hipMemcpyAsync(Au.data(), A_up, sizeof(float) * nup, hipMemcpyDeviceToHost, s));
+  if (has_down)
+    DTP_HIP(hipMemcpyAsync(Ad.data(), A_down, sizeof(float) * ndown, hipMemcpyDeviceToHost, s));
+  DTP_HIP(hipStreamSynchronize(s));
+  std::vector<int64_t> Qu(nup), Qd(ndown);
+  for (int i = 0; i < N; ++i) {
+    st = encode_unit_mass(Au.data() + (size_t)i * G * I, (int64_t)G * I, Qu.data() + (size_t)i * G * I);
+    if (st != DTP_OK) return fail(st, "layer %d up affinity: %s", i, dtp_last_error());
+    if (has_down && i + 1 < N) {
+      st = encode_unit_mass(Ad.data() + (size_t)i * I * G, (int64_t)I * G, Qd.data() + (size_t)i * I * G);
+      if (st != DTP_OK) return fail(st, "layer %d down affinity: %s", i, dtp_last_error());
+    }
+  }
+
+  // Device copies of the codes for the head step.
+  ScoreWorkspace ws;
+  st = score_workspace_create(&ws, N, G, I, L);
+  if (st != DTP_OK) {
+    score_workspace_destroy(&ws);
+    return st;
+  }
+  struct WsGuard {
+    ScoreWorkspace* w;
+    ~WsGuard() { score_workspace_destroy(w); }
+  } guard{&ws};
+  DevBuf qu_dev, qd_dev, nu_dev;
+  DTP_HIP(hipMalloc(&qu_dev.p, sizeof(int64_t) * nup));
+  DTP_HIP(hipMalloc(&nu_dev.p, sizeof(int32_t) * (size_t)N * I));
+  DTP_HIP(hipMemcpyAsync(qu_dev.p, Qu.data(), sizeof(int64_t) * nup, hipMemcpyHostToDevice, s));
+  if (has_down) {
+    DTP_HIP(hipMalloc(&qd_dev.p, sizeof(int64_t) * ndown));
+    DTP_HIP(hipMemcpyAsync(qd_dev.p, Qd.data(), sizeof(int64_t) * ndown, hipMemcpyHostToDevice, s));
+  }
+  const std::vector<uint8_t> table = enumerate_partitions(G, L);
+
+  // Contiguous start.
+  std::vector<int32_t> hs((size_t)N * G), nus((size_t)N * I);
+  for (int i = 0; i < N; ++i) {
+    for (int g = 0; g < G; ++g) hs[(size_t)i * G + g] = g / (G / L);
+    for (int k = 0; k < I; ++k) nus[(size_t)i * I + k] = k / (I / L);
+  }
+  auto moves = [&](int i) { return opt.layer_mask == nullptr || opt.layer_mask[i] != 0; };
+  const bool minimise = opt.minimise != 0;
+  std::vector<int64_t> best(N);
+  int64_t J_prev = 0;
+  int sweep = 0;
+  while (sweep < opt.max_sweeps) {
+    ++sweep;
+    if (!opt.freeze_neurons) {
+      // Neuron block: layers are independent given the heads; solve them in parallel.
+      const unsigned hw = std::max(1u, std::thread::hardware_concurrency());
+      const int nthreads = (int)std::min<unsigned>(hw, (unsigned)N);
+      std::vector<std::thread> pool;
+      for (int t = 0; t < nthreads; ++t) {
+        pool.emplace_back([&, t]() {
+          std::vector<int64_t> M;
+          for (int i = t; i < N; i += nthreads) {
+            if (!moves(i)) continue;
+            const bool dn = has_down && i + 1 < N;
+            neuron_gain(G, I, L, Qu.data() + (size_t)i * G * I, hs.data() + (size_t)i * G,
+                        dn ? Qd.data() + (size_t)i * I * G : nullptr,
+                        dn ? hs.data() + (size_t)(i + 1) * G : nullptr, minimise, &M);
+            balanced_assign_exact(I, L, M.data(), nus.data() + (size_t)i * I, nullptr);
+          }
+        });
+      }
+      for (auto& th : pool) th.join();
+    }
+    if (!opt.freeze_heads) {
+      DTP_HIP(hipMemcpyAsync(nu_dev.p, nus.data(), sizeof(int32_t) * (size_t)N * I,
+                             hipMemcpyHostToDevice, s));
+      st = launch_partition_scores(ws, (const int64_t*)qu_dev.p, (const int32_t*)nu_dev.p,
+                                   (const int64_t*)qd_dev.p, (const int32_t*)nu_dev.p,
+                                   minimise ? 1 : 0, s);
+      if (st != DTP_OK) return st;
+      DTP_HIP(hipMemcpyAsync(best.data(), ws.best, sizeof(int64_t) * N, hipMemcpyDeviceToHost, s));
+      DTP_HIP(hipStreamSynchronize(s));
+      for (int i = 0; i < N; ++i) {
+        if (!moves(i)) continue;
+        DTP_CHECK(best[i] >= 0 && best[i] < P, DTP_ERR_HIP, "partition scoring returned rank %lld",
+                  (long long)best[i]);
+        for (int g = 0; g < G; ++g) hs[(size_t)i * G + g] = table[(size_t)best[i] * G + g];
+      }
+    }
+    const int64_t Jc = objective_int(N, G, I, Qu, Qd, has_down, hs, nus);
+    const bool improved = sweep == 1 || (minimise ? Jc < J_prev : Jc > J_prev);
+    J_prev = Jc;
+    if (!improved) break;
+  }
+  std::memcpy(h, hs.data(), sizeof(int32_t) * hs.size());
+  std::memcpy(nu, nus.data(), sizeof(int32_t) * nus.size());
+  *J_fixed = J_prev;
+  *J = (double)J_prev / (double)(int64_t(1) << kFracBits);
+  *sweeps = sweep;
+  return DTP_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,751 @@
+// First-order head-to-neuron affinity on MI355X (gfx950): Section 3 of the paper,
+// "Affinity scores", score FO, accumulated over a stream of calibration tokens.
+//
+// For token t with residual x (entering the FFN pre-norm), r = sqrt(mean(x^2) + eps),
+// gain gamma, neuron k's pre-activations g_k = w^g_k . (gamma x / r) and u_k likewise,
+// and head h's normalised piece p_h = gamma (a_h W_o^(h)) / r, the damage is
+//   Delta_hk = silu'(g_k) u_k (p_h . w^g_k) + silu(g_k) (p_h . w^u_k)
+// and the layer's raw score is A[g, k] = ||w^d_k||^2 sum_t sum_{h in g} Delta_hk^2.
+//
+// Re-association (exact up to rounding): p_h . w_k = (a_h . F_h[:, k]) / r with the folded
+// matrix F_h = W_o^(h) diag(gamma) W^T of shape [dh, I].  So per token
+//   Delta_hk = c1_k (a_h . Fg_h[:, k]) + c2_k (a_h . Fu_h[:, k]),
+//   c1_k = silu'(g_k) u_k / r,   c2_k = silu(g_k) / r,
+// and the whole layer is one long contraction per (token tile, neuron tile): first
+// [x] x [gamma W_gate | gamma W_up]^T over d (operating point), then, for every head,
+// [a_h] x [Fg_h | Fu_h] over dh, with a register epilogue after each head.
+//
+// Kernels of the bf16 path:
+//   prep_gate_up_kernel   W' = W diag(gamma), gate and up rows interleaved per neuron tile
+//   transpose_kernel      W_o^T, so both fold operands are K-contiguous
+//   fold_kernel           F = W' W_o (MFMA)
+//   down_norm_kernel      n_d[k] = ||w^d_k||^2
+//   rms_kernel            1/r per token
+//   affinity_bf16_kernel  the fused operating point + per-head damage + token reduction
+//   reduce_splits_kernel  deterministic fp64 sum of the per-split partials into A
+// The bf16 weights of a neuron tile form one K-contiguous operand of 128 rows (64 gate,
+// 64 up) and d + H*dh columns: [W' | F_0 | F_1 | ... | F_{H-1}].  The token operand is the
+// matching concatenation [x | a_0 | ... | a_{H-1}] read straight from the caller's x and
+// attn, so the fused kernel is one contraction over d + H*dh with epilogues at the
+// operating-point and head boundaries.
+// The fp32 path (dtype DTP_F32) runs the same decomposition with plain FMA kernels.
+#include <cmath>
+#include <vector>
+
+#include "dtp_internal.h"
+
+namespace dtp {
+namespace {
+
+typedef __attribute__((ext_vector_type(8))) __bf16 bf16x8;
+typedef __attribute__((ext_vector_type(16))) float f32x16;
+typedef __attribute__((ext_vector_type(4))) uint32_t u32x4;
+
+constexpr int kBM = 128;          // tokens per block tile: 4 waves x 32 rows
+constexpr int kBN = 64;           // neurons per block tile
+constexpr int kCols = 2 * kBN;    // MFMA columns per tile: 64 gate | 64 up
+constexpr int kKC = 32;           // contraction depth per LDS stage of the fold
+constexpr int kLdsRow = kKC + 8;  // bf16 per LDS row
+constexpr int kThreads = 256;
+constexpr int kWaves = kThreads / 64;
+constexpr int kSliceTokens = 1 << 18;  // tokens per internal slice (size of the 1/r buffer)
+constexpr int kMaxSplits = 128;        // token splits per launch (size of the partials)
+constexpr int kTargetBlocks = 3072;    // aim for this many blocks per launch
+
+__device__ inline float bf16_to_f32(uint16_t b) { return __uint_as_float((uint32_t)b << 16); }
+
+__device__ inline uint16_t f32_to_bf16(float f) {
+  uint32_t u = __float_as_uint(f);
+  if ((u & 0x7fffffffu) > 0x7f800000u) return 0x7fc0;  // NaN stays NaN
+  u += 0x7fffu + ((u >> 16) & 1u);                      // round to nearest even
+  return (uint16_t)(u >> 16);
+}
+
+template <typename T>
+__device__ inline float load_f32(const T* p, int64_t i);
+template <>
+__device__ inline float load_f32<uint16_t>(const uint16_t* p, int64_t i) { return bf16_to_f32(p[i]); }
+template <>
+__device__ inline float load_f32<float>(const float* p, int64_t i) { return p[i]; }
+
+// ------------------------------------------------------------------ tile staging (bf16)
+// A stage is 128 rows x KC contraction columns; each of the 256 threads moves KC/16
+// segments of 16 bytes (8 bf16) from global memory into registers, then into LDS.
+template <int KC>
+struct Stage {
+  u32x4 v[KC / 16];
+};
+
+template <int KC>
+__device__ inline void stage_load(Stage<KC>& s, const uint16_t* __restrict__ base, int64_t ld,
+                                  int rows_valid, int k0, int k_valid) {
+  constexpr int kSegs = KC / 8;              // 16-byte segments per row
+  constexpr int kRowsPerPass = kThreads / kSegs;
+  const int t = threadIdx.x;
+  const int k = k0 + (t % kSegs) * 8;
+#pragma unroll
+  for (int j = 0; j < KC / 16; ++j) {
+    const int row = t / kSegs + kRowsPerPass * j;
+    if (row < rows_valid && k < k_valid)
+      s.v[j] = *reinterpret_cast<const u32x4*>(base + (int64_t)row * ld + k);
+    else
+      s.v[j] = u32x4{0u, 0u, 0u, 0u};
+  }
+}
+
+template <int KC>
+__device__ inline void stage_store(const Stage<KC>& s, uint16_t* lds) {
+  constexpr int kSegs = KC / 8;
+  constexpr int kRowsPerPass = kThreads / kSegs;
+  const int t = threadIdx.x;
+#pragma unroll
+  for (int j = 0; j < KC / 16; ++j) {
+    const int row = t / kSegs + kRowsPerPass * j;
+    *reinterpret_cast<u32x4*>(lds + row * (KC + 8) + (t % kSegs) * 8) = s.v[j];
+  }
+}
+
+// One stage of MFMA work: the wave's 32 rows of A against the 128 columns of B, with LDS
+// rows of KC + 8 bf16 (the 16 bytes of padding spread consecutive rows over the banks).
+// v_mfma_f32_32x32x16_bf16: lane l feeds row (l % 32) of A / column (l % 32) of B with the
+// 8 contraction elements starting at 8 * (l / 32).
+template <int KC>
+__device__ inline void mfma_stage(const uint16_t* As, const uint16_t* Bs, f32x16 (&acc)[4],
+                                  int wave, int lane) {
+  constexpr int kRow = KC + 8;
+  const int r = lane & 31;
+  const int kh = (lane >> 5) * 8;
+#pragma unroll
+  for (int ks = 0; ks < KC; ks += 16) {
+    const bf16x8 a = *reinterpret_cast<const bf16x8*>(As + (wave * 32 + r) * kRow + ks + kh);
+#pragma unroll
+    for (int b = 0; b < 4; ++b) {
+      const bf16x8 bb = *reinterpret_cast<const bf16x8*>(Bs + (b * 32 + r) * kRow + ks + kh);
+      acc[b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, bb, acc[b], 0, 0, 0);
+    }
+  }
+}
+
+// Row (within the wave's 32) held by accumulator element i of lane l.
+__device__ inline int acc_row(int i, int lane) { return 8 * (i >> 2) + 4 * (lane >> 5) + (i & 3); }
+
+// ------------------------------------------------------------------ weight preparation
+// out[tile*128 + c][j] (row stride ld) = W[k][j] * gamma[j], k = tile*64 + c%64,
+// W = gate for c < 64 else up; rows of padding neurons are zero.
+template <typename T>
+__global__ void prep_gate_up_kernel(const T* __restrict__ w_gate, const T* __restrict__ w_up,
+                                    const T* __restrict__ gamma, int I, int d, int n_tiles,
+                                    int64_t ld, T* __restrict__ out) {
+  const int64_t total = (int64_t)n_tiles * kCols * d;
+  for (int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; idx < total;
+       idx += (int64_t)gridDim.x * blockDim.x) {
+    const int j = (int)(idx % d);
+    const int64_t rowi = idx / d;
+    const int c = (int)(rowi % kCols);
+    const int k = (int)(rowi / kCols) * kBN + (c % kBN);
+    float v = 0.0f;
+    if (k < I) v = load_f32(c < kBN ? w_gate : w_up, (int64_t)k * d + j) * load_f32(gamma, j);
+    if constexpr (sizeof(T) == 2)
+      out[rowi * ld + j] = f32_to_bf16(v);
+    else
+      out[rowi * ld + j] = v;
+  }
+}
+
+// out[n][j] = in[j][n] for in of shape [rows, cols].
+__global__ void transpose_kernel(const uint16_t* __restrict__ in, int rows, int cols,
+                                 uint16_t* __restrict__ out) {
+  __shared__ uint16_t tile[32][33];
+  const int c0 = blockIdx.x * 32, r0 = blockIdx.y * 32;
+  const int tx = threadIdx.x & 31, ty = threadIdx.x >> 5;  // 256 threads: 32 x 8
+  for (int y = ty; y < 32; y += 8) {
+    const int r = r0 + y, c = c0 + tx;
+    tile[y][tx] = (r < rows && c < cols) ? in[(int64_t)r * cols + c] : (uint16_t)0;
+  }
+  __syncthreads();
+  for (int y = ty; y < 32; y += 8) {
+    const int c = c0 + y, r = r0 + tx;
+    if (c < cols && r < rows) out[(int64_t)c * rows + r] = tile[tx][y];
+  }
+}
+
+// wcat[m][d + n] = sum_j wcat[m][j] * woT[n][j] for m < M = n_tiles*128, n < N = H*dh:
+// the folded F_h[:, k] of every head h (n = h*dh + e), next to W' in the same row.
+__global__ void __launch_bounds__(kThreads)
+fold_kernel(uint16_t* __restrict__ wcat, const uint16_t* __restrict__ woT, int N, int d,
+            int64_t ld) {
+  __shared__ __attribute__((aligned(16))) uint16_t As[2][kBM * kLdsRow];
+  __shared__ __attribute__((aligned(16))) uint16_t Bs[2][kCols * kLdsRow];
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int m0 = blockIdx.x * kBM, n0 = blockIdx.y * kCols;
+  const uint16_t* a_base = wcat + (int64_t)m0 * ld;
+  const uint16_t* b_base = woT + (int64_t)n0 * d;
+  const int n_valid = N - n0;
+  f32x16 acc[4];
+#pragma unroll
+  for (int b = 0; b < 4; ++b) acc[b] = f32x16{};
+  const int nch = (d + kKC - 1) / kKC;
+  Stage<kKC> sa, sb;
+  stage_load<kKC>(sa, a_base, ld, kBM, 0, d);
+  stage_load<kKC>(sb, b_base, d, n_valid, 0, d);
+  stage_store<kKC>(sa, As[0]);
+  stage_store<kKC>(sb, Bs[0]);
+  __syncthreads();
+  for (int q = 0; q < nch; ++q) {
+    const int buf = q & 1;
+    if (q + 1 < nch) {
+      stage_load<kKC>(sa, a_base, ld, kBM, (q + 1) * kKC, d);
+      stage_load<kKC>(sb, b_base, d, n_valid, (q + 1) * kKC, d);
+    }
+    mfma_stage<kKC>(As[buf], Bs[buf], acc, wave, lane);
+    if (q + 1 < nch) {
+      stage_store<kKC>(sa, As[buf ^ 1]);
+      stage_store<kKC>(sb, Bs[buf ^ 1]);
+    }
+    __syncthreads();
+  }
+#pragma unroll
+  for (int b = 0; b < 4; ++b) {
+    const int n = n0 + b * 32 + (lane & 31);
+    if (n >= N) continue;
+#pragma unroll
+    for (int i = 0; i < 16; ++i) {
+      const int m = m0 + wave * 32 + acc_row(i, lane);
+      wcat[(int64_t)m * ld + d + n] = f32_to_bf16(acc[b][i]);
+    }
+  }
+}
+
+// fp32 fold: F[h][gu][k][e] = sum_j W_o[j][h*dh + e] * gamma[j] * W_gu[k][j]
+__global__ void fold_f32_kernel(const float* __restrict__ w_o, const float* __restrict__ gamma,
+                                const float* __restrict__ w_gate, const float* __restrict__ w_up,
+                                int d, int I, int H, int dh, float* __restrict__ fold) {
+  const int64_t total = (int64_t)H * 2 * I * dh;
+  for (int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; idx < total;
+       idx += (int64_t)gridDim.x * blockDim.x) {
+    const int e = (int)(idx % dh);
+    const int k = (int)((idx / dh) % I);
+    const int gu = (int)((idx / ((int64_t)dh * I)) % 2);
+    const int h = (int)(idx / ((int64_t)dh * I * 2));
+    const float* w = (gu == 0 ? w_gate : w_up) + (int64_t)k * d;
+    float s = 0.0f;
+    for (int j = 0; j < d; ++j) s = fmaf(w_o[(int64_t)j * H * dh + h * dh + e] * gamma[j], w[j], s);
+    fold[idx] = s;
+  }
+}
+
+template <typename T>
+__global__ void down_norm_kernel(const T* __restrict__ w_down, int d, int I, int I_pad,
+                                 float* __restrict__ nd) {
+  const int k = blockIdx.x * blockDim.x + threadIdx.x;
+  if (k >= I_pad) return;
+  float s = 0.0f;
+  if (k < I)
+    for (int j = 0; j < d; ++j) {
+      const float v = load_f32(w_down, (int64_t)j * I + k);
+      s = fmaf(v, v, s);
+    }
+  nd[k] = s;
+}
+
+// ------------------------------------------------------------------ per-token scalars
+// rinv[t] = 1 / sqrt(mean_j x[t][j]^2 + eps); one wavefront per token.
+template <typename T>
+__global__ void __launch_bounds__(256)
+rms_kernel(const T* __restrict__ x, int64_t T_tokens, int d, float eps, float* __restrict__ rinv) {
+  const int64_t t = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63;
+  if (t >= T_tokens) return;  // whole wavefronts exit together
+  const T* row = x + t * d;
+  float s = 0.0f;
+  for (int j = lane; j < d; j += 64) {
+    const float v = load_f32(row, j);
+    s = fmaf(v, v, s);
+  }
+  for (int off = 32; off > 0; off >>= 1) s += __shfl_xor(s, off, 64);
+  if (lane == 0) rinv[t] = 1.0f / sqrtf(s / (float)d + eps);
+}
+
+// ------------------------------------------------------------------ fused affinity (bf16)
+struct AffinityArgs {
+  const uint16_t* x;      // [T][d]
+  const uint16_t* attn;   // [T][H*dh]
+  const uint16_t* wcat;   // [n_tiles*128][Kt], Kt = d + H*dh
+  const float* rinv;      // [T]
+  const float* nd;        // [I_pad]
+  float* partial;         // [splits][G][I_pad]
+  int T, d, H, G, dh, n_tiles, splits, I_pad, Kt;
+};
+
+// Block = (neuron tile of 64, token split).  For every 128-token tile of its split the
+// block runs one contraction over Kt = d + H*dh in stages of KC:
+//   stages [0, d/KC)          acc = [x] . [W'_gate | W'_up]^T          -> c1, c2 in registers
+//   each next dh/KC stages    acc = [a_h] . [Fg_h | Fu_h]^T            -> Delta^2 column sums
+// Wave w owns token rows 32w..32w+31 and all 128 columns (4 MFMA blocks: gate 0-31,
+// gate 32-63, up 0-31, up 32-63), so c1/c2 and both damage terms of a (token, neuron)
+// pair sit in the same lane.  Column sums are kept per lane over its 16 rows, folded
+// across the two half-waves after the last query head of each KV group, and banked in
+// LDS per (wave, group); the block writes the fixed-order sum over its waves times
+// ||w^d_k||^2 to its split's partial.
+template <int KC>
+__global__ void __launch_bounds__(kThreads, 2)
+affinity_bf16_kernel(AffinityArgs p) {
+  constexpr int kRow = KC + 8;
+  __shared__ __attribute__((aligned(16))) uint16_t As[2][kBM * kRow];
+  __shared__ __attribute__((aligned(16))) uint16_t Bs[2][kCols * kRow];
+  extern __shared__ float red[];  // [kWaves][G][kBN]
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int tile = blockIdx.x / p.splits;
+  const int split = blockIdx.x % p.splits;
+  const int HD = p.H * p.dh;
+  const int hpg = p.H / p.G;
+
+  for (int i = threadIdx.x; i < kWaves * p.G * kBN; i += kThreads) red[i] = 0.0f;
+
+  const int mtiles = (p.T + kBM - 1) / kBM;
+  const int per = (mtiles + p.splits - 1) / p.splits;
+  const int mt_begin = split * per;
+  const int mt_end = min(mtiles, mt_begin + per);
+  const int nq1 = p.d / KC;   // operating-point stages
+  const int nqh = p.dh / KC;  // stages per head
+  const int nq = nq1 + p.H * nqh;
+  const uint16_t* w_tile = p.wcat + (int64_t)tile * kCols * p.Kt;
+  __syncthreads();
+
+  for (int mt = mt_begin; mt < mt_end; ++mt) {
+    const int m0 = mt * kBM;
+    const int rows_valid = min(kBM, p.T - m0);
+    const uint16_t* x_tile = p.x + (int64_t)m0 * p.d;
+    const uint16_t* a_tile = p.attn + (int64_t)m0 * HD;
+    auto load = [&](int q, Stage<KC>& sa, Stage<KC>& sb) {
+      const int k0 = q * KC;
+      if (q < nq1)
+        stage_load<KC>(sa, x_tile, p.d, rows_valid, k0, p.d);
+      else
+        stage_load<KC>(sa, a_tile, HD, rows_valid, k0 - p.d, HD);
+      stage_load<KC>(sb, w_tile, p.Kt, kCols, k0, p.Kt);
+    };
+
+    f32x16 acc[4];
+#pragma unroll
+    for (int b = 0; b < 4; ++b) acc[b] = f32x16{};
+    float c1[2][16], c2[2][16];
+    float colsum[2] = {0.0f, 0.0f};
+
+    Stage<KC> sa, sb;
+    load(0, sa, sb);
+    stage_store<KC>(sa, As[0]);
+    stage_store<KC>(sb, Bs[0]);
+    __syncthreads();
+    int head_stage = 0;  // stages done of the current head
+    int h = 0;
+    for (int q = 0; q < nq; ++q) {
+      const int buf = q & 1;
+      if (q + 1 < nq) load(q + 1, sa, sb);
+      mfma_stage<KC>(As[buf], Bs[buf], acc, wave, lane);
+      if (q == nq1 - 1) {
+        // Operating point: g, u -> c1 = silu'(g) u / r, c2 = silu(g) / r.
+#pragma unroll
+        for (int i = 0; i < 16; ++i) {
+          const int row = m0 + wave * 32 + acc_row(i, lane);
+          const float ri = row < p.T ? p.rinv[row] : 0.0f;
+#pragma unroll
+          for (int j = 0; j < 2; ++j) {
+            const float g = acc[j][i] * ri;
+            const float u = acc[2 + j][i] * ri;
+            const float sg = 1.0f / (1.0f + __expf(-g));
+            c2[j][i] = g * sg * ri;
+            c1[j][i] = sg * (1.0f + g * (1.0f - sg)) * u * ri;
+          }
+        }
+#pragma unroll
+        for (int b = 0; b < 4; ++b) acc[b] = f32x16{};
+      } else if (q >= nq1 && ++head_stage == nqh) {
+        // Head h done: Delta = c1 (a_h . Fg) + c2 (a_h . Fu); sum Delta^2 over the rows.
+#pragma unroll
+        for (int j = 0; j < 2; ++j)
+#pragma unroll
+          for (int i = 0; i < 16; ++i) {
+            const float dl = c1[j][i] * acc[j][i] + c2[j][i] * acc[2 + j][i];
+            colsum[j] = fmaf(dl, dl, colsum[j]);
+          }
+#pragma unroll
+        for (int b = 0; b < 4; ++b) acc[b] = f32x16{};
+        head_stage = 0;
+        if (h % hpg == hpg - 1) {
+          // Last query head of its KV group: fold the two half-waves and bank the sums.
+          const float s0 = colsum[0] + __shfl_xor(colsum[0], 32, 64);
+          const float s1 = colsum[1] + __shfl_xor(colsum[1], 32, 64);
+          red[(wave * p.G + h / hpg) * kBN + lane] += (lane < 32) ? s0 : s1;
+          colsum[0] = colsum[1] = 0.0f;
+        }
+        ++h;
+      }
+      if (q + 1 < nq) {
+        stage_store<KC>(sa, As[buf ^ 1]);
+        stage_store<KC>(sb, Bs[buf ^ 1]);
+      }
+      __syncthreads();
+    }
+  }
+
+  // Sum the waves in a fixed order and scale by ||w^d_k||^2.
+  for (int i = threadIdx.x; i < p.G * kBN; i += kThreads) {
+    const int g = i / kBN, k = i % kBN;
+    float s = 0.0f;
+    for (int w = 0; w < kWaves; ++w) s += red[(w * p.G + g) * kBN + k];
+    const int n = tile * kBN + k;
+    p.partial[((int64_t)split * p.G + g) * p.I_pad + n] = s * p.nd[n];
+  }
+}
+
+// ------------------------------------------------------------------ fused affinity (fp32)
+// One thread per (neuron, token lane); heads visited group by group.
+struct AffinityF32Args {
+  const float* x;      // [T][d]
+  const float* attn;   // [T][H*dh]
+  const float* wgu;    // [n_tiles*128][d] gamma-scaled gate | up rows per tile
+  const float* fold;   // [H][2][I][dh]
+  const float* rinv;
+  const float* nd;
+  float* partial;      // [splits][G][I_pad]
+  int T, d, H, G, dh, I, I_pad, splits;
+};
+
+__global__ void __launch_bounds__(256)
+affinity_f32_kernel(AffinityF32Args p) {
+  // blockDim = 256 = 4 token lanes x 64 neurons of one tile
+  __shared__ float red[4][kMaxAffinityGroups][kBN];
+  const int kl = threadIdx.x & 63, tl = threadIdx.x >> 6;
+  const int tile = blockIdx.x / p.splits, split = blockIdx.x % p.splits;
+  const int k = tile * kBN + kl;
+  const int HD = p.H * p.dh, hpg = p.H / p.G;
+  const int per = (p.T + p.splits - 1) / p.splits;
+  const int t0 = split * per, t1 = min(p.T, t0 + per);
+  float acc[kMaxAffinityGroups];
+  for (int g = 0; g < p.G; ++g) acc[g] = 0.0f;
+  if (k < p.I) {
+    const float* wg = p.wgu + (int64_t)tile * kCols * p.d + (int64_t)kl * p.d;
+    const float* wu = wg + (int64_t)kBN * p.d;
+    for (int t = t0 + tl; t < t1; t += 4) {
+      const float* xr = p.x + (int64_t)t * p.d;
+      const float ri = p.rinv[t];
+      float g = 0.0f, u = 0.0f;
+      for (int j = 0; j < p.d; ++j) {
+        g = fmaf(wg[j], xr[j], g);
+        u = fmaf(wu[j], xr[j], u);
+      }
+      g *= ri;
+      u *= ri;
+      const float sg = 1.0f / (1.0f + expf(-g));
+      const float cc2 = g * sg * ri;
+      const float cc1 = sg * (1.0f + g * (1.0f - sg)) * u * ri;
+      for (int h = 0; h < p.H; ++h) {
+        const float* ar = p.attn + (int64_t)t * HD + h * p.dh;
+        const float* fg = p.fold + (((int64_t)h * 2 + 0) * p.I + k) * p.dh;
+        const float* fu = p.fold + (((int64_t)h * 2 + 1) * p.I + k) * p.dh;
+        float pg = 0.0f, pu = 0.0f;
+        for (int e = 0; e < p.dh; ++e) {
+          pg = fmaf(ar[e], fg[e], pg);
+          pu = fmaf(ar[e], fu[e], pu);
+        }
+        const float dl = cc1 * pg + cc2 * pu;
+        acc[h / hpg] = fmaf(dl, dl, acc[h / hpg]);
+      }
+    }
+  }
+  for (int g = 0; g < p.G; ++g) red[tl][g][kl] = acc[g];
+  __syncthreads();
+  for (int i = threadIdx.x; i < p.G * kBN; i += 256) {
+    const int g = i / kBN, kk = i % kBN;
+    const float s = red[0][g][kk] + red[1][g][kk] + red[2][g][kk] + red[3][g][kk];
+    const int n = tile * kBN + kk;
+    p.partial[((int64_t)split * p.G + g) * p.I_pad + n] = s * p.nd[n];
+  }
+}
+
+// A[g][k] += sum_s partial[s][g][k], in fp64 and in split order.
+__global__ void reduce_splits_kernel(const float* __restrict__ partial, int splits, int G, int I,
+                                     int I_pad, float* __restrict__ A) {
+  const int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (idx >= (int64_t)G * I) return;
+  const int g = (int)(idx / I), k = (int)(idx % I);
+  double s = (double)A[idx];
+  for (int sp = 0; sp < splits; ++sp) s += (double)partial[((int64_t)sp * G + g) * I_pad + k];
+  A[idx] = (float)s;
+}
+
+inline unsigned grid_for(int64_t n, int threads) {
+  const int64_t b = (n + threads - 1) / threads;
+  return (unsigned)std::min<int64_t>(b, 1 << 20);
+}
+
+bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
+
+}  // namespace
+}  // namespace dtp
+
+using namespace dtp;
+
+struct dtp_layer_s {
+  dtp_layer_desc desc;
+  int device = 0;
+  int n_tiles = 0, I_pad = 0, Kt = 0;
+  bool has_weights = false;
+  void* w = nullptr;       // bf16 wcat [n_tiles*128][d + H*dh]; f32 W' [n_tiles*128][d]
+  void* woT = nullptr;     // bf16 [H*dh][d]: W_o^T, operand of the fold
+  float* fold32 = nullptr;   // f32 path: [H][2][I][dh]
+  float* nd = nullptr;       // [I_pad]
+  float* rinv = nullptr;     // [kSliceTokens]
+  float* partial = nullptr;  // [kMaxSplits][G][I_pad]
+  bool profiling = false;
+  std::vector<std::pair<hipEvent_t, hipEvent_t>> events;
+};
+
+namespace {
+
+void layer_free(dtp_layer L) {
+  void* bufs[] = {L->w, L->woT, L->fold32, L->nd, L->rinv, L->partial};
+  for (void* b : bufs)
+    if (b) (void)hipFree(b);
+  for (auto& e : L->events) {
+    (void)hipEventDestroy(e.first);
+    (void)hipEventDestroy(e.second);
+  }
+  delete L;
+}
+
+dtp_status check_device(dtp_layer L) {
+  int dev = -1;
+  DTP_HIP(hipGetDevice(&dev));
+  DTP_CHECK(dev == L->device, DTP_ERR_INVALID_ARG,
+            "layer was created on device %d but device %d is current", L->device, dev);
+  return DTP_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+dtp_status dtp_layer_create(const dtp_layer_desc* desc, dtp_layer* out) {
+  clear_error();
+  DTP_CHECK(desc != nullptr && out != nullptr, DTP_ERR_INVALID_ARG, "desc or out is NULL");
+  const dtp_layer_desc& d = *desc;
+  DTP_CHECK(d.d_model > 0 && d.n_neurons > 0 && d.n_q_heads > 0 && d.n_kv_groups > 0 &&
+                d.head_dim > 0,
+            DTP_ERR_INVALID_ARG, "every size must be positive (d=%d I=%d H=%d G=%d dh=%d)",
+            d.d_model, d.n_neurons, d.n_q_heads, d.n_kv_groups, d.head_dim);
+  DTP_CHECK(d.n_q_heads % d.n_kv_groups == 0, DTP_ERR_INVALID_ARG,
+            "H=%d is not a multiple of G=%d", d.n_q_heads, d.n_kv_groups);
+  DTP_CHECK(d.n_kv_groups <= kMaxAffinityGroups, DTP_ERR_UNSUPPORTED, "G=%d exceeds %d",
+            d.n_kv_groups, kMaxAffinityGroups);
+  DTP_CHECK(d.head_dim % 16 == 0, DTP_ERR_INVALID_ARG, "head_dim=%d is not a multiple of 16",
+            d.head_dim);
+  DTP_CHECK(d.d_model % 16 == 0, DTP_ERR_INVALID_ARG, "d_model=%d is not a multiple of 16",
+            d.d_model);
+  DTP_CHECK(d.d_model <= 65536 && d.n_neurons <= (1 << 20) &&
+                (int64_t)d.n_q_heads * d.head_dim <= 65536,
+            DTP_ERR_UNSUPPORTED, "shape too large (d <= 65536, I <= 2^20, H*dh <= 65536)");
+  DTP_CHECK(std::isfinite(d.rms_eps) && d.rms_eps >= 0.0f, DTP_ERR_INVALID_ARG,
+            "rms_eps=%g must be finite and >= 0", (double)d.rms_eps);
+  DTP_CHECK(d.dtype == DTP_BF16 || d.dtype == DTP_F32, DTP_ERR_UNSUPPORTED, "dtype %d",
+            d.dtype);
+  dtp_layer L = new (std::nothrow) dtp_layer_s();
+  DTP_CHECK(L != nullptr, DTP_ERR_NO_MEMORY, "host allocation failed");
+  L->desc = d;
+  hipError_t e = hipGetDevice(&L->device);
+  L->n_tiles = (d.n_neurons + kBN - 1) / kBN;
+  L->I_pad = L->n_tiles * kBN;
+  const int64_t HD = (int64_t)d.n_q_heads * d.head_dim;
+  const size_t rows = (size_t)L->n_tiles * kCols;
+  if (d.dtype == DTP_BF16) {
+    L->Kt = d.d_model + (int)HD;
+    if (e == hipSuccess) e = hipMalloc(&L->w, 2 * rows * L->Kt);
+    if (e == hipSuccess) e = hipMalloc(&L->woT, 2 * (size_t)HD * d.d_model);
+  } else {
+    L->Kt = d.d_model;
+    if (e == hipSuccess) e = hipMalloc(&L->w, 4 * rows * d.d_model);
+    if (e == hipSuccess) e = hipMalloc(&L->fold32, 4 * (size_t)HD * 2 * d.n_neurons);
+  }
+  if (e == hipSuccess) e = hipMalloc(&L->nd, 4 * (size_t)L->I_pad);
+  if (e == hipSuccess) e = hipMalloc(&L->rinv, 4 * (size_t)kSliceTokens);
+  if (e == hipSuccess)
+    e = hipMalloc(&L->partial, 4 * (size_t)kMaxSplits * d.n_kv_groups * L->I_pad);
+  if (e != hipSuccess) {
+    layer_free(L);
+    return fail(e == hipErrorOutOfMemory ? DTP_ERR_NO_MEMORY : DTP_ERR_HIP,
+                "layer allocation failed: %s", hipGetErrorString(e));
+  }
+  *out = L;
+  return DTP_OK;
+}
+
+dtp_status dtp_layer_destroy(dtp_layer layer) {
+  clear_error();
+  if (layer) layer_free(layer);
+  return DTP_OK;
+}
+
+dtp_status dtp_layer_set_weights(dtp_layer L, const void* w_o, const void* gamma,
+                                 const void* w_gate, const void* w_up, const void* w_down,
+                                 void* stream) {
+  clear_error();
+  DTP_CHECK(L != nullptr, DTP_ERR_INVALID_ARG, "layer is NULL");
+  DTP_CHECK(w_o && gamma && w_gate && w_up && w_down, DTP_ERR_INVALID_ARG,
+            "a weight pointer is NULL");
+  dtp_status st = check_device(L);
+  if (st != DTP_OK) return st;
+  hipStream_t s = (hipStream_t)stream;
+  const dtp_layer_desc& d = L->desc;
+  const int H = d.n_q_heads, dh = d.head_dim, HD = H * dh, I = d.n_neurons, dm = d.d_model;
+  const int64_t n = (int64_t)L->n_tiles * kCols * dm;
+  if (d.dtype == DTP_BF16) {
+    prep_gate_up_kernel<uint16_t><<<grid_for(n, 256), 256, 0, s>>>(
+        (const uint16_t*)w_gate, (const uint16_t*)w_up, (const uint16_t*)gamma, I, dm, L->n_tiles,
+        L->Kt, (uint16_t*)L->w);
+    DTP_HIP(hipGetLastError());
+    dim3 tg((HD + 31) / 32, (dm + 31) / 32);
+    transpose_kernel<<<tg, 256, 0, s>>>((const uint16_t*)w_o, dm, HD, (uint16_t*)L->woT);
+    DTP_HIP(hipGetLastError());
+    dim3 fg(L->n_tiles * kCols / kBM, (HD + kCols - 1) / kCols);
+    fold_kernel<<<fg, kThreads, 0, s>>>((uint16_t*)L->w, (const uint16_t*)L->woT, HD, dm, L->Kt);
+    DTP_HIP(hipGetLastError());
+    down_norm_kernel<uint16_t><<<grid_for(L->I_pad, 256), 256, 0, s>>>(
+        (const uint16_t*)w_down, dm, I, L->I_pad, L->nd);
+    DTP_HIP(hipGetLastError());
+  } else {
+    prep_gate_up_kernel<float><<<grid_for(n, 256), 256, 0, s>>>(
+        (const float*)w_gate, (const float*)w_up, (const float*)gamma, I, dm, L->n_tiles, dm,
+        (float*)L->w);
+    DTP_HIP(hipGetLastError());
+    const int64_t nf = (int64_t)H * 2 * I * dh;
+    fold_f32_kernel<<<grid_for(nf, 256), 256, 0, s>>>((const float*)w_o, (const float*)gamma,
+                                                       (const float*)w_gate, (const float*)w_up,
+                                                       dm, I, H, dh, L->fold32);
+    DTP_HIP(hipGetLastError());
+    down_norm_kernel<float><<<grid_for(L->I_pad, 256), 256, 0, s>>>((const float*)w_down, dm, I,
+                                                                     L->I_pad, L->nd);
+    DTP_HIP(hipGetLastError());
+  }
+  L->has_weights = true;
+  return DTP_OK;
+}
+
+dtp_status dtp_affinity_accumulate(dtp_layer L, const void* x, const void* attn, int64_t n_tokens,
+                                   float* A, void* stream) {
+  clear_error();
+  DTP_CHECK(L != nullptr, DTP_ERR_INVALID_ARG, "layer is NULL");
+  DTP_CHECK(n_tokens >= 0, DTP_ERR_INVALID_ARG, "n_tokens=%lld is negative", (long long)n_tokens);
+  if (n_tokens == 0) return DTP_OK;
+  DTP_CHECK(x && attn && A, DTP_ERR_INVALID_ARG, "x, attn or A is NULL");
+  DTP_CHECK(aligned16(x) && aligned16(attn), DTP_ERR_INVALID_ARG,
+            "x and attn must be 16-byte aligned");
+  DTP_CHECK(L->has_weights, DTP_ERR_INVALID_ARG, "dtp_layer_set_weights was not called");
+  dtp_status st = check_device(L);
+  if (st != DTP_OK) return st;
+  hipStream_t s = (hipStream_t)stream;
+  const dtp_layer_desc& d = L->desc;
+  const int H = d.n_q_heads, dh = d.head_dim, HD = H * dh, G = d.n_kv_groups;
+  const int I = d.n_neurons, dm = d.d_model;
+  const size_t esz = d.dtype == DTP_BF16 ? 2 : 4;
+  for (int64_t t0 = 0; t0 < n_tokens; t0 += kSliceTokens) {
+    const int T = (int)std::min<int64_t>(kSliceTokens, n_tokens - t0);
+    const char* xs = (const char*)x + esz * (size_t)t0 * dm;
+    const char* as = (const char*)attn + esz * (size_t)t0 * HD;
+    const unsigned rb = (unsigned)((T + 3) / 4);
+    if (d.dtype == DTP_BF16)
+      rms_kernel<uint16_t><<<rb, 256, 0, s>>>((const uint16_t*)xs, T, dm, d.rms_eps, L->rinv);
+    else
+      rms_kernel<float><<<rb, 256, 0, s>>>((const float*)xs, T, dm, d.rms_eps, L->rinv);
+    DTP_HIP(hipGetLastError());
+
+    int splits;
+    hipEvent_t e0 = nullptr, e1 = nullptr;
+    if (L->profiling) {
+      DTP_HIP(hipEventCreate(&e0));
+      DTP_HIP(hipEventCreate(&e1));
+      DTP_HIP(hipEventRecord(e0, s));
+    }
+    if (d.dtype == DTP_BF16) {
+      const int mtiles = (T + kBM - 1) / kBM;
+      splits = (kTargetBlocks + L->n_tiles - 1) / L->n_tiles;
+      splits = std::max(1, std::min(splits, std::min(mtiles, kMaxSplits)));
+      AffinityArgs p;
+      p.x = (const uint16_t*)xs;
+      p.attn = (const uint16_t*)as;
+      p.wcat = (const uint16_t*)L->w;
+      p.rinv = L->rinv;
+      p.nd = L->nd;
+      p.partial = L->partial;
+      p.T = T;
+      p.d = dm;
+      p.H = H;
+      p.G = G;
+      p.dh = dh;
+      p.n_tiles = L->n_tiles;
+      p.splits = splits;
+      p.I_pad = L->I_pad;
+      p.Kt = L->Kt;
+      const size_t shm = sizeof(float) * kWaves * G * kBN;
+      affinity_bf16_kernel<16><<<L->n_tiles * splits, kThreads, shm, s>>>(p);
+    } else {
+      splits = (kTargetBlocks / 4 + L->n_tiles - 1) / L->n_tiles;
+      splits = std::max(1, std::min(splits, std::min(T, kMaxSplits)));
+      AffinityF32Args p;
+      p.x = (const float*)xs;
+      p.attn = (const float*)as;
+      p.wgu = (const float*)L->w;
+      p.fold = L->fold32;
+      p.rinv = L->rinv;
+      p.nd = L->nd;
+      p.partial = L->partial;
+      p.T = T;
+      p.d = dm;
+      p.H = H;
+      p.G = G;
+      p.dh = dh;
+      p.I = I;
+      p.I_pad = L->I_pad;
+      p.splits = splits;
+      affinity_f32_kernel<<<L->n_tiles * splits, 256, 0, s>>>(p);
+    }
+    DTP_HIP(hipGetLastError());
+    if (L->profiling) {
+      DTP_HIP(hipEventRecord(e1, s));
+      L->events.emplace_back(e0, e1);
+    }
+    reduce_splits_kernel<<<grid_for((int64_t)G * I, 256), 256, 0, s>>>(L->partial, splits, G, I,
+                                                                       L->I_pad, A);
+    DTP_HIP(hipGetLastError());
+  }
+  return DTP_OK;
+}
+
+dtp_status dtp_layer_profile(dtp_layer L, int32_t enable) {
+  clear_error();
+  DTP_CHECK(L != nullptr, DTP_ERR_INVALID_ARG, "layer is NULL");
+  L->profiling = enable != 0;
+  return DTP_OK;
+}
+
+dtp_status dtp_layer_profile_read(dtp_layer L, double* total_ms, int64_t* launches) {
+  clear_error();
+  DTP_CHECK(L != nullptr && total_ms && launches, DTP_ERR_INVALID_ARG, "NULL argument");
+  double sum = 0.0;
+  for (auto& e : L->events) {
+    DTP_HIP(hipEventSynchronize(e.second));
+    float ms = 0.0f;
+    DTP_HIP(hipEventElapsedTime(&ms, e.first, e.second));
+    sum += ms;
+  }
+  *total_ms = sum;
+  *launches = (int64_t)L->events.size();
+  for (auto& e : L->events) {
+    (void)hipEventDestroy(e.first);
+    (void)hipEventDestroy(e.second);
+  }
+  L->events.clear();
+  return DTP_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,203 @@
+// Exact balanced neuron assignment (Section 3, "Optimiser", neuron step).
+//
+// Given the gain M[k][l] of putting neuron k on device l, find nu maximising
+// sum_k M[k][nu[k]] with exactly I/L neurons per device: a linear assignment with I/L
+// replicated slots per device.  The paper solves it approximately (dual ascent, a
+// capacity fix-up, pairwise swaps); this solver is exact.
+//
+// 1. Optimum.  Neurons are inserted one at a time, each along a best augmenting path of
+//    the current optimal partial assignment (the successive-shortest-path method of the
+//    assignment problem, one row at a time).  Because there are only L devices, a path is
+//    a walk over devices: the new neuron enters device a0, then for every hop a -> b the
+//    neuron of a with the largest M[j][b] - M[j][a] moves to b, and the walk ends at a
+//    device with a free slot.  Best moves per device pair come from lazy max-heaps, and
+//    the longest walk is Bellman-Ford over the L devices (no gaining cycle exists while
+//    the partial assignment is optimal).
+// 2. Canonical optimum.  Device prices lambda are longest-path distances in the exchange
+//    graph of the optimum; every optimal assignment uses only "tight" pairs
+//    (k, l) with M[k][l] - lambda_l = max_l' (M[k][l'] - lambda_l') (complementary
+//    slackness), and every balanced assignment on tight pairs is optimal.  The answer is
+//    the lexicographically smallest of them: neurons in index order take the smallest
+//    tight device that leaves a feasible completion, feasibility being Hall's condition
+//    over device subsets, evaluated by a subset-sum over tight-set masks.
+#include <algorithm>
+#include <queue>
+#include <utility>
+#include <vector>
+
+#include "dtp_internal.h"
+
+namespace dtp {
+
+namespace {
+
+using Entry = std::pair<int64_t, int32_t>;  // (gain of moving j from a to b, j)
+
+struct PairHeaps {
+  int L;
+  std::vector<std::priority_queue<Entry>> heap;  // [a * L + b]
+  explicit PairHeaps(int L_) : L(L_), heap((size_t)L_ * L_) {}
+
+  void add(const int64_t* M, int j, int a) {
+    const int64_t* m = M + (size_t)j * L;
+    for (int b = 0; b < L; ++b)
+      if (b != a) heap[(size_t)a * L + b].push(Entry(m[b] - m[a], j));
+  }
+  // Best (gain, neuron) currently on device a for a move to b; false if a is empty.
+  bool top(int a, int b, const std::vector<int32_t>& nu, Entry* out) {
+    auto& h = heap[(size_t)a * L + b];
+    while (!h.empty() && nu[h.top().second] != a) h.pop();
+    if (h.empty()) return false;
+    *out = h.top();
+    return true;
+  }
+};
+
+void optimal_by_insertion(int I, int L, const int64_t* M, std::vector<int32_t>& nu) {
+  const int cap = I / L;
+  std::vector<int> count(L, 0);
+  PairHeaps heaps(L);
+  std::vector<int64_t> dist(L);
+  std::vector<int> pred(L);
+  std::vector<Entry> edge((size_t)L * L);
+  std::vector<char> has_edge((size_t)L * L);
+  for (int k = 0; k < I; ++k) {
+    for (int a = 0; a < L; ++a)
+      for (int b = 0; b < L; ++b) {
+        const size_t e = (size_t)a * L + b;
+        has_edge[e] = (a != b) && heaps.top(a, b, nu, &edge[e]);
+      }
+    const int64_t* mk = M + (size_t)k * L;
+    for (int a = 0; a < L; ++a) {
+      dist[a] = mk[a];
+      pred[a] = -1;
+    }
+    for (int round = 0; round + 1 < L; ++round) {
+      bool changed = false;
+      for (int a = 0; a < L; ++a)
+        for (int b = 0; b < L; ++b) {
+          const size_t e = (size_t)a * L + b;
+          if (!has_edge[e]) continue;
+          const int64_t cand = dist[a] + edge[e].first;
+          if (cand > dist[b]) {
+            dist[b] = cand;
+            pred[b] = a;
+            changed = true;
+          }
+        }
+      if (!changed) break;
+    }
+    int end = -1;
+    for (int b = 0; b < L; ++b)
+      if (count[b] < cap && (end < 0 || dist[b] > dist[end])) end = b;
+    // Collect the moves along the walk before touching the heaps.
+    std::vector<std::pair<int32_t, int>> moves;
+    int b = end;
+    while (pred[b] >= 0) {
+      const int a = pred[b];
+      moves.emplace_back(edge[(size_t)a * L + b].second, b);
+      b = a;
+    }
+    const int entry = b;
+    for (const auto& mv : moves) {
+      nu[mv.first] = mv.second;
+      heaps.add(M, mv.first, mv.second);
+    }
+    nu[k] = entry;
+    heaps.add(M, k, entry);
+    ++count[end];
+  }
+}
+
+void canonicalise(int I, int L, const int64_t* M, std::vector<int32_t>& nu) {
+  // Exchange graph of the optimum and prices by longest paths from a zero source.
+  std::vector<int64_t> w((size_t)L * L, 0);
+  std::vector<char> has((size_t)L * L, 0);
+  for (int j = 0; j < I; ++j) {
+    const int a = nu[j];
+    const int64_t* m = M + (size_t)j * L;
+    for (int b = 0; b < L; ++b) {
+      if (b == a) continue;
+      const size_t e = (size_t)a * L + b;
+      const int64_t gain = m[b] - m[a];
+      if (!has[e] || gain > w[e]) {
+        w[e] = gain;
+        has[e] = 1;
+      }
+    }
+  }
+  std::vector<int64_t> lam(L, 0);
+  for (int round = 0; round < L; ++round)
+    for (int a = 0; a < L; ++a)
+      for (int b = 0; b < L; ++b) {
+        const size_t e = (size_t)a * L + b;
+        if (has[e] && lam[a] + w[e] > lam[b]) lam[b] = lam[a] + w[e];
+      }
+  // Tight-set mask of every neuron.
+  const int nmask = 1 << L;
+  std::vector<uint32_t> mask(I);
+  std::vector<int64_t> cnt(nmask, 0);
+  for (int k = 0; k < I; ++k) {
+    const int64_t* m = M + (size_t)k * L;
+    int64_t best = m[0] - lam[0];
+    for (int l = 1; l < L; ++l) best = std::max(best, m[l] - lam[l]);
+    uint32_t mk = 0;
+    for (int l = 0; l < L; ++l)
+      if (m[l] - lam[l] == best) mk |= 1u << l;
+    mask[k] = mk;
+    ++cnt[mk];
+  }
+  std::vector<int64_t> cap(L, I / L), need(nmask);
+  auto feasible = [&]() {
+    // need[S] = number of remaining neurons whose tight set lies inside S
+    for (int s = 0; s < nmask; ++s) need[s] = cnt[s];
+    for (int l = 0; l < L; ++l)
+      for (int s = 0; s < nmask; ++s)
+        if (s >> l & 1) need[s] += need[s ^ (1 << l)];
+    for (int s = 1; s < nmask; ++s) {
+      int64_t have = 0;
+      for (int l = 0; l < L; ++l)
+        if (s >> l & 1) have += cap[l];
+      if (need[s] > have) return false;
+    }
+    return true;
+  };
+  for (int k = 0; k < I; ++k) {
+    --cnt[mask[k]];
+    if ((mask[k] & (mask[k] - 1)) == 0) {  // one tight device: the invariant keeps it feasible
+      const int l = __builtin_ctz(mask[k]);
+      --cap[l];
+      nu[k] = l;
+      continue;
+    }
+    for (int l = 0; l < L; ++l) {
+      if (!(mask[k] >> l & 1) || cap[l] == 0) continue;
+      --cap[l];
+      if (feasible()) {
+        nu[k] = l;
+        break;
+      }
+      ++cap[l];
+    }
+  }
+}
+
+}  // namespace
+
+void balanced_assign_exact(int I, int L, const int64_t* M, int32_t* nu_out, int64_t* value) {
+  std::vector<int32_t> nu(I, -1);
+  if (L == 1) {
+    std::fill(nu.begin(), nu.end(), 0);
+  } else {
+    optimal_by_insertion(I, L, M, nu);
+    canonicalise(I, L, M, nu);
+  }
+  int64_t v = 0;
+  for (int k = 0; k < I; ++k) {
+    nu_out[k] = nu[k];
+    v += M[(size_t)k * L + nu[k]];
+  }
+  if (value) *value = v;
+}
+
+}  // namespace dtp

@@ -1,0 +1,67 @@
+// Internal declarations shared by the translation units of libdtp.so.
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <cstdint>
+#include <string>
+#include <vector>
+
+#include "dtp.h"
+
+namespace dtp {
+
+// Records a thread-local message for dtp_last_error() and returns `s`.
+dtp_status fail(dtp_status s, const char* fmt, ...) __attribute__((format(printf, 2, 3)));
+void clear_error();
+
+#define DTP_HIP(call)                                                                 \
+  do {                                                                                \
+    hipError_t e_ = (call);                                                           \
+    if (e_ != hipSuccess)                                                             \
+      return ::dtp::fail(DTP_ERR_HIP, "%s failed: %s (%s:%d)", #call,                 \
+                         hipGetErrorString(e_), __FILE__, __LINE__);                  \
+  } while (0)
+
+#define DTP_CHECK(cond, status, ...)                                                  \
+  do {                                                                                \
+    if (!(cond)) return ::dtp::fail((status), __VA_ARGS__);                           \
+  } while (0)
+
+constexpr int kMaxGroups = 64;        // partition scoring: one lane per KV group
+constexpr int kMaxAffinityGroups = 32;  // affinity kernel: per-group sums kept in LDS
+constexpr int kMaxAssignDevices = 8;  // exact assignment: Hall checks over 2^L subsets
+constexpr int64_t kMaxPartitions = int64_t(1) << 24;
+constexpr int kFracBits = 48;
+constexpr int kMantBits = 40;
+
+// ---- unit-mass fixed point (encode.cpp)
+dtp_status encode_unit_mass(const float* A, int64_t n, int64_t* Q);
+
+// ---- labelled balanced partitions (partitions.cpp)
+int64_t count_partitions(int G, int L);               // -1 if invalid or > 2^62
+std::vector<uint8_t> enumerate_partitions(int G, int L);  // [P][G], lexicographic
+bool unrank_partition(int G, int L, int64_t rank, int32_t* h);
+
+// ---- exact balanced assignment (assign.cpp).  M is [I][L] row-major.
+// Returns the lexicographically smallest assignment maximising sum_k M[k][nu[k]].
+void balanced_assign_exact(int I, int L, const int64_t* M, int32_t* nu, int64_t* value);
+
+// ---- GPU partition scoring (scores.hip)
+struct ScoreWorkspace {
+  int N = 0, G = 0, I = 0, L = 0;
+  int64_t P = 0;
+  uint8_t* table = nullptr;   // dev [P][G]
+  int64_t* C = nullptr;       // dev [N][G][L]
+  int64_t* scores = nullptr;  // dev [N][P]
+  int64_t* best = nullptr;    // dev [N]
+};
+dtp_status score_workspace_create(ScoreWorkspace* ws, int N, int G, int I, int L);
+void score_workspace_destroy(ScoreWorkspace* ws);
+// Q_up dev [N][G][I]; nu dev [N][I]; Q_down dev [N-1][I][G] or null (layer i uses
+// Q_down[i-1] with nu[i-1]).  Enqueues C, scores and best on `stream`.
+dtp_status launch_partition_scores(const ScoreWorkspace& ws, const int64_t* Q_up,
+                                   const int32_t* nu, const int64_t* Q_down,
+                                   const int32_t* nu_down, int minimise, hipStream_t stream);
+
+}  // namespace dtp

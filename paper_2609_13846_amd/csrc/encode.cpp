@@ -1,0 +1,45 @@
+// Unit-mass normalisation of an affinity matrix as exact fixed point.
+//
+// The paper normalises every affinity matrix to unit mass before summing co-located
+// entries into the objective J (Section 3, "Objective").  To make J, the head-partition
+// scores and the neuron gains independent of summation order, the library carries the
+// normalised matrix as integers:
+//   E   = floor(log2 max A)
+//   q_i = floor(A_i * 2^(40 - E))        exact: A_i is an fp32 value, q_i < 2^41
+//   Q_i = floor(q_i * 2^48 / sum_j q_j)  128-bit intermediate
+// so sum_i Q_i lies in (2^48 - n, 2^48] and J = (sum of co-located Q) / 2^48.
+#include <cmath>
+#include <cstring>
+
+#include "dtp_internal.h"
+
+namespace dtp {
+
+dtp_status encode_unit_mass(const float* A, int64_t n, int64_t* Q) {
+  float amax = 0.0f;
+  for (int64_t i = 0; i < n; ++i) {
+    const float a = A[i];
+    if (!std::isfinite(a) || a < 0.0f)
+      return fail(DTP_ERR_DEGENERATE, "affinity entry %lld is %g (must be finite and >= 0)",
+                  (long long)i, (double)a);
+    if (a > amax) amax = a;
+  }
+  if (!(amax > 0.0f)) return fail(DTP_ERR_DEGENERATE, "affinity matrix is all zero");
+  int e = 0;
+  std::frexp(amax, &e);  // amax = m * 2^e, m in [0.5, 1)
+  const int E = e - 1;   // amax in [2^E, 2^(E+1))
+  const int shift = kMantBits - E;
+  unsigned __int128 S = 0;
+  for (int64_t i = 0; i < n; ++i) {
+    const double q = std::floor(std::ldexp((double)A[i], shift));
+    Q[i] = (int64_t)q;  // temporarily q_i
+    S += (unsigned __int128)(uint64_t)Q[i];
+  }
+  for (int64_t i = 0; i < n; ++i) {
+    const unsigned __int128 num = (unsigned __int128)(uint64_t)Q[i] << kFracBits;
+    Q[i] = (int64_t)(num / S);
+  }
+  return DTP_OK;
+}
+
+}  // namespace dtp

@@ -1,0 +1,162 @@
+// Head step on the GPU (Section 3, "Optimiser"): score every labelled balanced partition
+// of a layer's KV groups given the neighbouring neuron assignments.
+//
+// The objective is linear in h_i once nu_{i-1} and nu_i are fixed, so
+//   score(h) = sum_g C[g, h(g)],
+//   C[g, l]  = sum_{k: nu_i(k)=l} Q_up_i[g, k] + sum_{k: nu_{i-1}(k)=l} Q_down_{i-1}[k, g].
+// All quantities are int64 fixed-point codes, so sums are exact in any order.
+//
+// Kernels (all over N layers at once):
+//   head_gain_kernel      one block per (layer, group): C[g, :] by a block reduction
+//   partition_score_kernel one wavefront per (layer, partition): lane g adds C[g, h(g)]
+//   best_partition_kernel one block per layer: best score, lowest rank on ties
+#include "dtp_internal.h"
+
+namespace dtp {
+
+namespace {
+
+constexpr int kGainThreads = 256;
+constexpr int kMaxDevices = 64;
+
+__device__ inline int64_t wave_sum_i64(int64_t v) {
+  for (int off = 32; off > 0; off >>= 1) {
+    const int lo = __shfl_xor((int)(uint32_t)(uint64_t)v, off, 64);
+    const int hi = __shfl_xor((int)(uint32_t)((uint64_t)v >> 32), off, 64);
+    v += (int64_t)(((uint64_t)(uint32_t)hi << 32) | (uint64_t)(uint32_t)lo);
+  }
+  return v;
+}
+
+__global__ void __launch_bounds__(kGainThreads)
+head_gain_kernel(const int64_t* __restrict__ Q_up, const int32_t* __restrict__ nu,
+                 const int64_t* __restrict__ Q_down, const int32_t* __restrict__ nu_down,
+                 int G, int I, int L, int64_t* __restrict__ C) {
+  __shared__ int64_t part[kGainThreads / 64][kMaxDevices];
+  const int layer = blockIdx.x / G;
+  const int g = blockIdx.x % G;
+  const int lane = threadIdx.x & 63;
+  const int wave = threadIdx.x >> 6;
+  const int64_t* qu = Q_up + ((size_t)layer * G + g) * I;
+  const int32_t* nl = nu + (size_t)layer * I;
+  const bool down = Q_down != nullptr && layer > 0;
+  const int64_t* qd = down ? Q_down + (size_t)(layer - 1) * I * G : nullptr;
+  const int32_t* nd = down ? nu_down + (size_t)(layer - 1) * I : nullptr;
+  for (int l = 0; l < L; ++l) {
+    int64_t acc = 0;
+    for (int k = threadIdx.x; k < I; k += kGainThreads) {
+      if (nl[k] == l) acc += qu[k];
+      if (down && nd[k] == l) acc += qd[(size_t)k * G + g];
+    }
+    acc = wave_sum_i64(acc);
+    if (lane == 0) part[wave][l] = acc;
+  }
+  __syncthreads();
+  for (int l = threadIdx.x; l < L; l += kGainThreads) {
+    int64_t s = 0;
+    for (int w = 0; w < kGainThreads / 64; ++w) s += part[w][l];
+    C[((size_t)layer * G + g) * L + l] = s;
+  }
+}
+
+// One wavefront per (layer, partition); lanes index KV groups (G <= 64).
+__global__ void __launch_bounds__(256)
+partition_score_kernel(const uint8_t* __restrict__ table, const int64_t* __restrict__ C,
+                       int N, int G, int L, int64_t P, int64_t* __restrict__ scores) {
+  const int64_t wid = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) >> 6;
+  const int lane = threadIdx.x & 63;
+  if (wid >= (int64_t)N * P) return;  // whole wavefronts exit together
+  const int layer = (int)(wid / P);
+  const int64_t p = wid % P;
+  int64_t v = 0;
+  if (lane < G) {
+    const int dev = table[p * G + lane];
+    v = C[((size_t)layer * G + lane) * L + dev];
+  }
+  v = wave_sum_i64(v);
+  if (lane == 0) scores[(size_t)layer * P + p] = v;
+}
+
+__device__ inline bool better(int64_t s, int64_t r, int64_t bs, int64_t br, int minimise) {
+  if (s != bs) return minimise ? (s < bs) : (s > bs);
+  return r < br;
+}
+
+__global__ void __launch_bounds__(256)
+best_partition_kernel(const int64_t* __restrict__ scores, int64_t P, int minimise,
+                      int64_t* __restrict__ best) {
+  __shared__ int64_t ss[256];
+  __shared__ int64_t sr[256];
+  const int layer = blockIdx.x;
+  const int64_t* sc = scores + (size_t)layer * P;
+  int64_t bs = 0, br = -1;
+  for (int64_t p = threadIdx.x; p < P; p += blockDim.x) {
+    if (br < 0 || better(sc[p], p, bs, br, minimise)) {
+      bs = sc[p];
+      br = p;
+    }
+  }
+  ss[threadIdx.x] = bs;
+  sr[threadIdx.x] = br;
+  __syncthreads();
+  for (int step = 128; step > 0; step >>= 1) {
+    if (threadIdx.x < step) {
+      const int o = threadIdx.x + step;
+      if (sr[o] >= 0 && (sr[threadIdx.x] < 0 ||
+                         better(ss[o], sr[o], ss[threadIdx.x], sr[threadIdx.x], minimise))) {
+        ss[threadIdx.x] = ss[o];
+        sr[threadIdx.x] = sr[o];
+      }
+    }
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) best[layer] = sr[0];
+}
+
+}  // namespace
+
+dtp_status score_workspace_create(ScoreWorkspace* ws, int N, int G, int I, int L) {
+  ws->N = N;
+  ws->G = G;
+  ws->I = I;
+  ws->L = L;
+  ws->P = count_partitions(G, L);
+  DTP_CHECK(ws->P > 0 && ws->P <= kMaxPartitions, DTP_ERR_UNSUPPORTED,
+            "%lld partitions of %d groups over %d devices exceed the limit of %lld",
+            (long long)ws->P, G, L, (long long)kMaxPartitions);
+  const std::vector<uint8_t> table = enumerate_partitions(G, L);
+  DTP_HIP(hipMalloc(&ws->table, table.size()));
+  DTP_HIP(hipMalloc(&ws->C, sizeof(int64_t) * (size_t)N * G * L));
+  DTP_HIP(hipMalloc(&ws->scores, sizeof(int64_t) * (size_t)N * ws->P));
+  DTP_HIP(hipMalloc(&ws->best, sizeof(int64_t) * (size_t)N));
+  DTP_HIP(hipMemcpy(ws->table, table.data(), table.size(), hipMemcpyHostToDevice));
+  return DTP_OK;
+}
+
+void score_workspace_destroy(ScoreWorkspace* ws) {
+  if (ws->table) (void)hipFree(ws->table);
+  if (ws->C) (void)hipFree(ws->C);
+  if (ws->scores) (void)hipFree(ws->scores);
+  if (ws->best) (void)hipFree(ws->best);
+  *ws = ScoreWorkspace();
+}
+
+dtp_status launch_partition_scores(const ScoreWorkspace& ws, const int64_t* Q_up,
+                                   const int32_t* nu, const int64_t* Q_down,
+                                   const int32_t* nu_down, int minimise, hipStream_t stream) {
+  DTP_CHECK(ws.L <= kMaxDevices && ws.G <= kMaxGroups, DTP_ERR_UNSUPPORTED,
+            "partition scoring supports G <= %d and L <= %d", kMaxGroups, kMaxDevices);
+  head_gain_kernel<<<ws.N * ws.G, kGainThreads, 0, stream>>>(Q_up, nu, Q_down, nu_down, ws.G,
+                                                             ws.I, ws.L, ws.C);
+  DTP_HIP(hipGetLastError());
+  const int64_t waves = (int64_t)ws.N * ws.P;
+  const int64_t blocks = (waves + 3) / 4;
+  partition_score_kernel<<<(unsigned)blocks, 256, 0, stream>>>(ws.table, ws.C, ws.N, ws.G,
+                                                               ws.L, ws.P, ws.scores);
+  DTP_HIP(hipGetLastError());
+  best_partition_kernel<<<ws.N, 256, 0, stream>>>(ws.scores, ws.P, minimise, ws.best);
+  DTP_HIP(hipGetLastError());
+  return DTP_OK;
+}
+
+}  // namespace dtp

@@ -1,0 +1,214 @@
+"""ctypes binding of libdtp.so (declared in include/dtp.h), one Python function per C entry point.
+
+The functions carry the C names and only marshal arguments: device tensors are passed
+as ``tensor.data_ptr()`` together with the current HIP stream, host arrays as numpy
+buffers.  Every computation runs in the library.  A non-OK status raises ``DtpError``
+with the library's message.  If ``libdtp.so`` has not been built, loading fails loudly:
+there is no fallback.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import re
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libdtp.so")
+HEADER = os.path.join(os.path.dirname(_HERE), "include", "dtp.h")
+
+DTP_BF16 = 0
+DTP_F32 = 1
+DTP_OK, DTP_ERR_INVALID_ARG, DTP_ERR_UNSUPPORTED, DTP_ERR_DEGENERATE, DTP_ERR_NO_MEMORY, DTP_ERR_HIP = (
+    0, -1, -2, -3, -4, -5)
+
+
+class DtpError(RuntimeError):
+    def __init__(self, status: int, message: str):
+        super().__init__(message)
+        self.status = status
+
+
+class dtp_layer_desc(ctypes.Structure):
+    _fields_ = [("d_model", ctypes.c_int32), ("n_neurons", ctypes.c_int32),
+                ("n_q_heads", ctypes.c_int32), ("n_kv_groups", ctypes.c_int32),
+                ("head_dim", ctypes.c_int32), ("rms_eps", ctypes.c_float),
+                ("dtype", ctypes.c_int32)]
+
+
+class dtp_ca_options(ctypes.Structure):
+    _fields_ = [("max_sweeps", ctypes.c_int32), ("freeze_heads", ctypes.c_int32),
+                ("freeze_neurons", ctypes.c_int32), ("minimise", ctypes.c_int32),
+                ("layer_mask", ctypes.c_void_p)]
+
+
+_P = ctypes.c_void_p
+_I32 = ctypes.c_int32
+_I64 = ctypes.c_int64
+_SIGNATURES = {
+    "dtp_layer_create": (_I32, [ctypes.POINTER(dtp_layer_desc), ctypes.POINTER(_P)]),
+    "dtp_layer_destroy": (_I32, [_P]),
+    "dtp_layer_set_weights": (_I32, [_P, _P, _P, _P, _P, _P, _P]),
+    "dtp_affinity_accumulate": (_I32, [_P, _P, _P, _I64, _P, _P]),
+    "dtp_layer_profile": (_I32, [_P, _I32]),
+    "dtp_layer_profile_read": (_I32, [_P, ctypes.POINTER(ctypes.c_double), ctypes.POINTER(_I64)]),
+    "dtp_partition_count": (_I64, [_I32, _I32]),
+    "dtp_partition_unrank": (_I32, [_I32, _I32, _I64, _P]),
+    "dtp_encode_affinity": (_I32, [_P, _I64, _P]),
+    "dtp_partition_scores": (_I32, [_I32, _I32, _I32, _P, _P, _P, _P, _I32, _P, ctypes.POINTER(_I64), _P]),
+    "dtp_balanced_assign": (_I32, [_I32, _I32, _I32, _P, _P, _P, _P, _I32, _P, ctypes.POINTER(_I64)]),
+    "dtp_coordinate_ascent": (_I32, [_I32, _I32, _I32, _I32, _P, _P, ctypes.POINTER(dtp_ca_options),
+                                     _P, _P, ctypes.POINTER(_I64), ctypes.POINTER(ctypes.c_double),
+                                     ctypes.POINTER(_I32), _P]),
+    "dtp_status_string": (ctypes.c_char_p, [_I32]),
+    "dtp_last_error": (ctypes.c_char_p, []),
+}
+
+_lib = None
+
+
+def lib() -> ctypes.CDLL:
+    """The loaded library; raises if it has not been built."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise DtpError(DTP_ERR_UNSUPPORTED, f"{LIB_PATH} is missing: build it with "
+                           "`python -m paper_2609_13846_amd.build` (there is no fallback)")
+        l = ctypes.CDLL(LIB_PATH)
+        for name, (res, args) in _SIGNATURES.items():
+            fn = getattr(l, name)
+            fn.restype = res
+            fn.argtypes = args
+        _lib = l
+    return _lib
+
+
+def header_symbols() -> list:
+    """Names of the functions include/dtp.h declares."""
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(dtp_[a-z_]+)\s*\(", text)))
+
+
+def _check(status: int):
+    if status != DTP_OK:
+        l = lib()
+        raise DtpError(status, f"{l.dtp_status_string(status).decode()}: {l.dtp_last_error().decode()}")
+
+
+def _ptr(x):
+    """Address of a torch tensor, a numpy array, an int or None."""
+    if x is None:
+        return None
+    if isinstance(x, int):
+        return x
+    if isinstance(x, np.ndarray):
+        if not x.flags["C_CONTIGUOUS"]:
+            raise ValueError("numpy arrays must be C-contiguous")
+        return x.ctypes.data
+    if hasattr(x, "data_ptr"):
+        if not x.is_contiguous():
+            raise ValueError("tensors must be contiguous")
+        return x.data_ptr()
+    raise TypeError(f"cannot pass {type(x)!r} as a pointer")
+
+
+def _stream(stream):
+    if stream is not None:
+        return stream if isinstance(stream, int) else stream.cuda_stream
+    import torch
+    if torch.cuda.is_available() and torch.cuda.is_initialized():
+        return torch.cuda.current_stream().cuda_stream
+    return None
+
+
+# ----------------------------------------------------------------------------- affinity
+def dtp_layer_create(d_model, n_neurons, n_q_heads, n_kv_groups, head_dim, rms_eps, dtype):
+    desc = dtp_layer_desc(d_model, n_neurons, n_q_heads, n_kv_groups, head_dim, rms_eps, dtype)
+    h = _P()
+    _check(lib().dtp_layer_create(ctypes.byref(desc), ctypes.byref(h)))
+    return h.value
+
+
+def dtp_layer_destroy(layer):
+    _check(lib().dtp_layer_destroy(layer))
+
+
+def dtp_layer_set_weights(layer, w_o, gamma, w_gate, w_up, w_down, stream=None):
+    _check(lib().dtp_layer_set_weights(layer, _ptr(w_o), _ptr(gamma), _ptr(w_gate), _ptr(w_up),
+                                       _ptr(w_down), _stream(stream)))
+
+
+def dtp_affinity_accumulate(layer, x, attn, n_tokens, A, stream=None):
+    _check(lib().dtp_affinity_accumulate(layer, _ptr(x), _ptr(attn), int(n_tokens), _ptr(A),
+                                         _stream(stream)))
+
+
+def dtp_layer_profile(layer, enable):
+    _check(lib().dtp_layer_profile(layer, int(bool(enable))))
+
+
+def dtp_layer_profile_read(layer):
+    ms = ctypes.c_double()
+    n = _I64()
+    _check(lib().dtp_layer_profile_read(layer, ctypes.byref(ms), ctypes.byref(n)))
+    return ms.value, n.value
+
+
+# ----------------------------------------------------------------------------- layout
+def dtp_partition_count(G, L):
+    return int(lib().dtp_partition_count(G, L))
+
+
+def dtp_partition_unrank(G, L, rank):
+    h = np.zeros(max(G, 1), dtype=np.int32)
+    _check(lib().dtp_partition_unrank(G, L, int(rank), _ptr(h)))
+    return h[:G]
+
+
+def dtp_encode_affinity(A):
+    a = np.ascontiguousarray(A, dtype=np.float32)
+    q = np.zeros(a.shape, dtype=np.int64)
+    _check(lib().dtp_encode_affinity(_ptr(a), a.size, _ptr(q)))
+    return q
+
+
+def dtp_partition_scores(G, I, L, Q_up, nu, Q_down_prev=None, nu_prev=None, minimise=False,
+                         scores=None, stream=None):
+    """Q_up, nu (and Q_down_prev, nu_prev) and scores are device tensors; returns best rank."""
+    best = _I64()
+    _check(lib().dtp_partition_scores(G, I, L, _ptr(Q_up), _ptr(nu), _ptr(Q_down_prev),
+                                      _ptr(nu_prev), int(bool(minimise)), _ptr(scores),
+                                      ctypes.byref(best), _stream(stream)))
+    return best.value
+
+
+def dtp_balanced_assign(G, I, L, Q_up, h, Q_down=None, h_next=None, minimise=False):
+    """Host arrays in, (nu int32 [I], value) out."""
+    qu = np.ascontiguousarray(Q_up, dtype=np.int64)
+    hh = np.ascontiguousarray(h, dtype=np.int32)
+    qd = None if Q_down is None else np.ascontiguousarray(Q_down, dtype=np.int64)
+    hn = None if h_next is None else np.ascontiguousarray(h_next, dtype=np.int32)
+    nu = np.zeros(max(I, 1), dtype=np.int32)
+    val = _I64()
+    _check(lib().dtp_balanced_assign(G, I, L, _ptr(qu), _ptr(hh), _ptr(qd), _ptr(hn),
+                                     int(bool(minimise)), _ptr(nu), ctypes.byref(val)))
+    return nu[:I], val.value
+
+
+def dtp_coordinate_ascent(N, G, I, L, A_up, A_down=None, max_sweeps=64, freeze_heads=False,
+                          freeze_neurons=False, minimise=False, layer_mask=None, stream=None):
+    """A_up [N,G,I] (and A_down [N-1,I,G]) are device tensors; returns a dict of host results."""
+    mask = None if layer_mask is None else np.ascontiguousarray(layer_mask, dtype=np.uint8)
+    opt = dtp_ca_options(max_sweeps, int(freeze_heads), int(freeze_neurons), int(minimise),
+                         _ptr(mask))
+    h = np.zeros((N, G), dtype=np.int32)
+    nu = np.zeros((N, I), dtype=np.int32)
+    jf = _I64()
+    j = ctypes.c_double()
+    sw = _I32()
+    _check(lib().dtp_coordinate_ascent(N, G, I, L, _ptr(A_up), _ptr(A_down), ctypes.byref(opt),
+                                       _ptr(h), _ptr(nu), ctypes.byref(jf), ctypes.byref(j),
+                                       ctypes.byref(sw), _stream(stream)))
+    return {"h": h, "nu": nu, "J_fixed": jf.value, "J": j.value, "sweeps": sw.value}

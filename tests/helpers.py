@@ -1,0 +1,68 @@
+"""Shared plumbing of the GPU tests: upload seeded inputs, run the library, compare."""
+from __future__ import annotations
+
+import numpy as np
+
+from paper_2609_13846_amd import dtp, synth
+
+REL_TOL = 1e-2        # relative error allowed on entries above THRESH * max(A)
+THRESH = 1e-3
+
+
+def torch_dev(arr: np.ndarray, device="cuda"):
+    """Storage array (uint16 bf16 bits or float32) -> device tensor with the same bytes."""
+    import torch
+    if arr.dtype == np.uint16:
+        return torch.from_numpy(arr.view(np.int16).copy()).view(torch.bfloat16).to(device)
+    return torch.from_numpy(np.ascontiguousarray(arr)).to(device)
+
+
+def layer_for(wl: synth.Workload):
+    dt = dtp.DTP_BF16 if wl.dtype == "bf16" else dtp.DTP_F32
+    return dtp.dtp_layer_create(wl.d_model, wl.n_neurons, wl.n_q_heads, wl.n_kv_groups,
+                                wl.head_dim, wl.rms_eps, dt)
+
+
+def gpu_affinity(wl: synth.Workload, w: synth.LayerWeights, x: np.ndarray, a: np.ndarray,
+                 chunks=None, A0=None) -> np.ndarray:
+    """A [G, I] float32 from the library, accumulated over token chunks (sizes)."""
+    import torch
+    T = x.shape[0]
+    layer = layer_for(wl)
+    try:
+        dw = [torch_dev(v) for v in (w.w_o, w.gamma, w.w_gate, w.w_up, w.w_down)]
+        dtp.dtp_layer_set_weights(layer, *dw)
+        dx, da = torch_dev(x), torch_dev(a)
+        A = torch.zeros(wl.n_kv_groups, wl.n_neurons, dtype=torch.float32, device="cuda")
+        if A0 is not None:
+            A.copy_(torch.from_numpy(A0))
+        bounds = [0]
+        for c in (chunks or [T]):
+            bounds.append(bounds[-1] + c)
+        assert bounds[-1] == T
+        for t0, t1 in zip(bounds, bounds[1:]):
+            dtp.dtp_affinity_accumulate(layer, dx[t0:t1], da[t0:t1], t1 - t0, A)
+        torch.cuda.synchronize()
+        return A.cpu().numpy()
+    finally:
+        dtp.dtp_layer_destroy(layer)
+
+
+def oracle_inputs(w: synth.LayerWeights, x, a):
+    f = synth.to_f64
+    return dict(x=f(x), attn=f(a), w_o=f(w.w_o), gamma=f(w.gamma), w_gate=f(w.w_gate),
+                w_up=f(w.w_up), w_down=f(w.w_down))
+
+
+def assert_affinity_close(A_gpu: np.ndarray, A_ref: np.ndarray, rel=REL_TOL, thresh=THRESH):
+    """Relative error <= rel on entries above thresh * max; the rest within rel * thresh * max."""
+    A_gpu = np.asarray(A_gpu, dtype=np.float64)
+    assert A_gpu.shape == A_ref.shape
+    assert np.all(np.isfinite(A_gpu))
+    top = A_ref.max()
+    big = A_ref > thresh * top
+    err = np.abs(A_gpu - A_ref)
+    rel_err = err[big] / A_ref[big]
+    assert rel_err.max() <= rel, f"max rel err {rel_err.max():.3e} (mean {rel_err.mean():.3e})"
+    assert err[~big].max(initial=0.0) <= rel * thresh * top
+    return float(rel_err.max())

@@ -1,0 +1,116 @@
+"""The C ABI: the library loads on a machine without a GPU, exports every declared
+symbol, and rejects bad arguments on the host before any GPU work (no compute call on
+the GPU is made here)."""
+import ctypes
+
+import numpy as np
+import pytest
+
+from paper_2609_13846_amd import dtp
+
+
+def test_library_exports_every_declared_symbol():
+    lib = dtp.lib()
+    names = dtp.header_symbols()
+    assert len(names) >= 14
+    for n in names:
+        assert hasattr(lib, n), n
+    assert set(names) == set(dtp._SIGNATURES)
+
+
+def test_status_strings():
+    lib = dtp.lib()
+    for code, name in [(0, "DTP_OK"), (-1, "DTP_ERR_INVALID_ARG"), (-2, "DTP_ERR_UNSUPPORTED"),
+                       (-3, "DTP_ERR_DEGENERATE"), (-4, "DTP_ERR_NO_MEMORY"), (-5, "DTP_ERR_HIP")]:
+        assert lib.dtp_status_string(code).decode() == name
+
+
+def _expect(status, fn, *a, **k):
+    with pytest.raises(dtp.DtpError) as e:
+        fn(*a, **k)
+    assert e.value.status == status, str(e.value)
+    assert str(e.value)
+
+
+@pytest.mark.parametrize("bad", [
+    dict(d_model=0), dict(n_neurons=-1), dict(n_q_heads=6, n_kv_groups=4),
+    dict(head_dim=24), dict(d_model=72), dict(rms_eps=-1.0), dict(rms_eps=float("nan")),
+])
+def test_layer_create_rejects_bad_shapes(bad):
+    kw = dict(d_model=64, n_neurons=128, n_q_heads=8, n_kv_groups=4, head_dim=16, rms_eps=1e-6,
+              dtype=dtp.DTP_BF16)
+    kw.update(bad)
+    _expect(dtp.DTP_ERR_INVALID_ARG, dtp.dtp_layer_create, **kw)
+
+
+@pytest.mark.parametrize("bad", [dict(dtype=7), dict(n_kv_groups=64, n_q_heads=64)])
+def test_layer_create_unsupported(bad):
+    kw = dict(d_model=64, n_neurons=128, n_q_heads=8, n_kv_groups=4, head_dim=16, rms_eps=1e-6,
+              dtype=dtp.DTP_BF16)
+    kw.update(bad)
+    _expect(dtp.DTP_ERR_UNSUPPORTED, dtp.dtp_layer_create, **kw)
+
+
+def test_null_layer_arguments():
+    lib = dtp.lib()
+    assert lib.dtp_layer_create(None, None) == dtp.DTP_ERR_INVALID_ARG
+    assert lib.dtp_layer_destroy(None) == dtp.DTP_OK
+    assert lib.dtp_layer_set_weights(None, 1, 1, 1, 1, 1, None) == dtp.DTP_ERR_INVALID_ARG
+    assert lib.dtp_affinity_accumulate(None, 1, 1, 10, 1, None) == dtp.DTP_ERR_INVALID_ARG
+    assert lib.dtp_layer_profile(None, 1) == dtp.DTP_ERR_INVALID_ARG
+    assert "NULL" in lib.dtp_last_error().decode()
+
+
+def test_partition_count_and_unrank_arguments():
+    assert dtp.dtp_partition_count(8, 4) == 2520
+    assert dtp.dtp_partition_count(8, 3) == -1
+    assert dtp.dtp_partition_count(65, 5) == -1
+    assert dtp.dtp_partition_count(0, 1) == -1
+    assert dtp.dtp_partition_count(64, 4) == -1   # beyond 2^62
+    _expect(dtp.DTP_ERR_INVALID_ARG, dtp.dtp_partition_unrank, 8, 4, 2520)
+    _expect(dtp.DTP_ERR_INVALID_ARG, dtp.dtp_partition_unrank, 8, 4, -1)
+    _expect(dtp.DTP_ERR_INVALID_ARG, dtp.dtp_partition_unrank, 8, 3, 0)
+
+
+def test_encode_arguments():
+    _expect(dtp.DTP_ERR_DEGENERATE, dtp.dtp_encode_affinity, np.zeros(5, np.float32))
+    _expect(dtp.DTP_ERR_DEGENERATE, dtp.dtp_encode_affinity, np.array([1, -1], np.float32))
+    _expect(dtp.DTP_ERR_DEGENERATE, dtp.dtp_encode_affinity, np.array([1, np.inf], np.float32))
+    _expect(dtp.DTP_ERR_DEGENERATE, dtp.dtp_encode_affinity, np.array([np.nan], np.float32))
+    lib = dtp.lib()
+    assert lib.dtp_encode_affinity(None, 4, None) == dtp.DTP_ERR_INVALID_ARG
+    a = np.ones(4, np.float32)
+    q = np.zeros(4, np.int64)
+    assert lib.dtp_encode_affinity(a.ctypes.data, 0, q.ctypes.data) == dtp.DTP_ERR_INVALID_ARG
+
+
+def test_balanced_assign_arguments():
+    Q = np.ones((8, 16), np.int64)
+    h = np.arange(8) // 2
+    _expect(dtp.DTP_ERR_INVALID_ARG, dtp.dtp_balanced_assign, 8, 15, 4, Q, h)          # I % L
+    _expect(dtp.DTP_ERR_INVALID_ARG, dtp.dtp_balanced_assign, 8, 16, 3, Q, h)          # G % L
+    _expect(dtp.DTP_ERR_INVALID_ARG, dtp.dtp_balanced_assign, 8, 16, 4, Q, np.zeros(8))  # unbalanced
+    _expect(dtp.DTP_ERR_INVALID_ARG, dtp.dtp_balanced_assign, 8, 16, 4, Q, h + 4)      # not a device
+    _expect(dtp.DTP_ERR_UNSUPPORTED, dtp.dtp_balanced_assign, 16, 16, 16, np.ones((16, 16), np.int64),
+            np.arange(16))                                                                  # L > 8
+    _expect(dtp.DTP_ERR_INVALID_ARG, dtp.dtp_balanced_assign, 8, 16, 4, Q, h, Q_down=Q.T.copy())
+    lib = dtp.lib()
+    v = ctypes.c_int64()
+    assert lib.dtp_balanced_assign(8, 16, 4, None, None, None, None, 0, None, ctypes.byref(v)) == \
+        dtp.DTP_ERR_INVALID_ARG
+
+
+def test_partition_scores_and_ascent_arguments_checked_before_gpu():
+    lib = dtp.lib()
+    best = ctypes.c_int64()
+    assert lib.dtp_partition_scores(8, 16, 3, 1, 1, None, None, 0, 1, ctypes.byref(best), None) == \
+        dtp.DTP_ERR_INVALID_ARG
+    assert lib.dtp_partition_scores(8, 16, 4, None, 1, None, None, 0, 1, ctypes.byref(best), None) == \
+        dtp.DTP_ERR_INVALID_ARG
+    assert lib.dtp_partition_scores(8, 16, 4, 1, 1, 1, None, 0, 1, ctypes.byref(best), None) == \
+        dtp.DTP_ERR_INVALID_ARG
+    _expect(dtp.DTP_ERR_INVALID_ARG, dtp.dtp_coordinate_ascent, 0, 8, 16, 4, 1)
+    _expect(dtp.DTP_ERR_INVALID_ARG, dtp.dtp_coordinate_ascent, 2, 8, 18, 4, 1)
+    _expect(dtp.DTP_ERR_INVALID_ARG, dtp.dtp_coordinate_ascent, 1, 8, 16, 4, 1, A_down=1)
+    _expect(dtp.DTP_ERR_INVALID_ARG, dtp.dtp_coordinate_ascent, 2, 8, 16, 4, 1, max_sweeps=0)
+    _expect(dtp.DTP_ERR_UNSUPPORTED, dtp.dtp_coordinate_ascent, 2, 32, 32, 16, 1)

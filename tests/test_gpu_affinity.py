@@ -1,0 +1,120 @@
+"""GPU parity of the affinity accumulation against the fp64 oracle (through the C ABI).
+
+Bar: relative error <= 1e-2 on every entry above 1e-3 * max(A) (bf16 inputs, fp32
+accumulation); smaller entries within 1e-2 * 1e-3 * max(A) absolute.  Sizes are chosen so
+the oracle finishes in seconds while spanning several token and neuron tiles and a
+ragged token tail; the full Qwen3-0.6B-shaped layer (65,536 tokens, the benchmarked
+launch) is checked on sampled neurons the oracle computes one by one.
+"""
+import sys
+
+import numpy as np
+import pytest
+
+from oracle import affinity as orc
+from paper_2609_13846_amd import dtp, synth
+from tests import helpers as hp
+
+pytestmark = pytest.mark.gpu
+
+
+def announce(msg):
+    print(f"[gpu] {msg}", file=sys.stderr, flush=True)
+
+
+def case(name, T, layer=0, **shape):
+    wl = synth.shaped(synth.WORKLOADS[name], **shape) if shape else synth.WORKLOADS[name]
+    w = synth.host_weights(wl, layer)
+    x, a = synth.host_tokens(wl, layer, w, T)
+    return wl, w, x, a
+
+
+def oracle(wl, w, x, a, neurons=None):
+    return orc.affinity_folded(**hp.oracle_inputs(w, x, a), n_kv_groups=wl.n_kv_groups,
+                               eps=wl.rms_eps, neurons=neurons)
+
+
+@pytest.mark.parametrize("name,T,shape", [
+    ("tiny", 512, {}),
+    ("tiny", 37, {}),
+    ("qwen3-0.6b-layer", 300, {}),
+    ("danube3-500m", 257, {}),
+    ("qwen3-0.6b-layer", 200, dict(n_neurons=1000)),               # ragged neuron tile
+    ("qwen3-0.6b-layer", 130, dict(n_q_heads=2, n_kv_groups=1)),    # one group
+    ("qwen3-0.6b-layer", 129, dict(n_q_heads=8, n_kv_groups=8, head_dim=48)),  # H = G, dh % 32 = 16
+    ("danube3-500m", 64, dict(d_model=272, n_neurons=192)),         # d % 32 = 16
+])
+def test_affinity_matches_oracle(name, T, shape):
+    wl, w, x, a = case(name, T, **shape)
+    announce(f"affinity {name} T={T} {shape}")
+    A = hp.gpu_affinity(wl, w, x, a)
+    hp.assert_affinity_close(A, oracle(wl, w, x, a))
+
+
+def test_affinity_8b_class_sampled_neurons():
+    wl, w, x, a = case("8b-class-4layer", 200, layer=3)
+    announce("affinity 8b-class T=200 sampled neurons")
+    A = hp.gpu_affinity(wl, w, x, a)
+    cols = np.r_[0:64, 7000:7064, wl.n_neurons - 64:wl.n_neurons]
+    hp.assert_affinity_close(A[:, cols], oracle(wl, w, x, a, neurons=cols))
+
+
+def test_affinity_full_qwen_layer_sampled_neurons():
+    """65,536 tokens in one call (the benchmarked launch); the oracle checks 96 neurons."""
+    wl = synth.WORKLOADS["qwen3-0.6b-layer"]
+    w = synth.host_weights(wl, 0)
+    x, a = synth.host_tokens(wl, 0, w, wl.tokens)
+    announce("affinity qwen3-0.6b-layer T=65536 (full)")
+    A = hp.gpu_affinity(wl, w, x, a)
+    rng = np.random.default_rng(0)
+    cols = np.sort(np.concatenate([rng.choice(wl.n_neurons, 64, replace=False), [0, 63, 64, 3071]]))
+    hp.assert_affinity_close(A[:, cols], oracle(wl, w, x, a, neurons=cols))
+    assert np.all(A > 0)
+
+
+def test_empty_and_single_token():
+    wl, w, x, a = case("qwen3-0.6b-layer", 1)
+    announce("affinity T=0 and T=1")
+    A0 = np.full((wl.n_kv_groups, wl.n_neurons), 0.25, np.float32)
+    A = hp.gpu_affinity(wl, w, x[:0], a[:0], chunks=[0], A0=A0)
+    np.testing.assert_array_equal(A, A0)
+    A1 = hp.gpu_affinity(wl, w, x, a)
+    hp.assert_affinity_close(A1, oracle(wl, w, x, a))
+
+
+def test_deterministic_and_chunk_additive():
+    wl, w, x, a = case("qwen3-0.6b-layer", 1000)
+    announce("affinity determinism and chunks T=1000")
+    A1 = hp.gpu_affinity(wl, w, x, a)
+    A2 = hp.gpu_affinity(wl, w, x, a)
+    np.testing.assert_array_equal(A1, A2)
+    A3 = hp.gpu_affinity(wl, w, x, a, chunks=[384, 333, 283])
+    np.testing.assert_allclose(A3, A1, rtol=1e-5)
+
+
+@pytest.mark.parametrize("c", [2.0, 0.5])
+def test_power_of_two_head_scale_is_exact(c):
+    """Scaling the query heads of one KV group by 2^k scales its row by 4^k bit for bit
+    (bf16 inputs stay exact and fp32 sums scale exactly); other rows are untouched."""
+    wl, w, x, a = case("qwen3-0.6b-layer", 700)
+    announce(f"affinity head scale {c}")
+    A = hp.gpu_affinity(wl, w, x, a)
+    g = 3
+    hpg = wl.n_q_heads // wl.n_kv_groups
+    a2 = synth.to_f64(a).copy()
+    a2[:, g * hpg:(g + 1) * hpg] *= c
+    A2 = hp.gpu_affinity(wl, w, x, synth.store(a2, "bf16"))
+    np.testing.assert_array_equal(A2[g], A[g] * np.float32(c * c))
+    np.testing.assert_array_equal(np.delete(A2, g, 0), np.delete(A, g, 0))
+
+
+def test_neuron_permutation_equivariance():
+    wl, w, x, a = case("qwen3-0.6b-layer", 400)
+    announce("affinity neuron permutation")
+    perm = np.random.default_rng(5).permutation(wl.n_neurons)
+    w2 = synth.LayerWeights(w.w_o, w.gamma, w.w_gate[perm].copy(), w.w_up[perm].copy(),
+                            w.w_down[:, perm].copy(), w.outliers)
+    A = hp.gpu_affinity(wl, w, x, a)
+    A2 = hp.gpu_affinity(wl, w2, x, a)
+    # each (group, neuron) entry is computed independently of its tile position
+    np.testing.assert_array_equal(A2, A[:, perm])
