@@ -129,7 +129,7 @@ def main():
     ap.add_argument("--steps", type=int, default=10)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default="qwen3-0.6b-layer")
-    ap.add_argument("--cpu-sample-tokens", type=int, default=4096)
+    ap.add_argument("--cpu-sample-tokens", type=int, default=49152)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--full-model", action="store_true")
     args = ap.parse_args()

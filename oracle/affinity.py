@@ -138,3 +138,4 @@ def affinity_folded(x, attn, w_o, gamma, w_gate, w_up, w_down, n_kv_groups, eps,
             dlt = c1 * (attn[sl, h, :] @ fg[h]) + c2 * (attn[sl, h, :] @ fu[h])
             acc[h] += np.sum(dlt * dlt, axis=0)
     return _aggregate(acc, w_down, n_kv_groups)
+

@@ -227,3 +227,4 @@ def test_silu_prime_is_derivative():
     gt = torch.tensor(g, requires_grad=True)
     torch.nn.functional.silu(gt).sum().backward()
     np.testing.assert_allclose(orc.silu_prime(g), gt.grad.numpy(), rtol=1e-13, atol=1e-15)
+
