@@ -132,6 +132,8 @@ def main():
     ap.add_argument("--cpu-sample-tokens", type=int, default=49152)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--full-model", action="store_true")
+    ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
+                    help="only run a plain device copy of this many MiB (HBM counter scale)")
     args = ap.parse_args()
     if args.gpus != 1:
         print("bench.py measures one GPU: the shard count is a logical layout parameter and the "
@@ -144,6 +146,16 @@ def main():
 
     device = torch.device("cuda", 0)
     torch.cuda.set_device(device)
+    if args.copy_calibration:
+        n = args.copy_calibration << 20
+        src = torch.empty(n, dtype=torch.uint8, device=device).fill_(1)
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        print(json.dumps({"copy_calibration_bytes": n, "launches": 3}), flush=True)
+        return
     wl = synth.WORKLOADS[args.workload]
     L = wl.shards[0]
     T, G, I = wl.tokens, wl.n_kv_groups, wl.n_neurons

@@ -277,22 +277,87 @@ struct AffinityArgs {
   int T, d, H, G, dh, n_tiles, splits, I_pad, Kt;
 };
 
+// Contraction order inside a stage of KC columns.  Lane l of a wavefront serves token row
+// (or weight column) l % 32 and the half h = l / 32 of the stage; its k-step s covers stage
+// columns h*KC/2 + 8s .. +7.  Any assignment of contraction indices to (half, k-step)
+// yields the same sums as long as both operands follow it; this one gives every lane one
+// contiguous run of KC bytes of its token row per stage, loaded straight into registers.
+template <int KC>
+struct TokenFrag {
+  u32x4 v[KC / 16];
+};
+
+template <int KC>
+__device__ inline void load_tokens(TokenFrag<KC>& f, const uint16_t* __restrict__ src, bool valid) {
+#pragma unroll
+  for (int s = 0; s < KC / 16; ++s)
+    f.v[s] = valid ? *reinterpret_cast<const u32x4*>(src + 8 * s) : u32x4{0u, 0u, 0u, 0u};
+}
+
+// A stage of the weight tile: 128 columns x KC contraction elements, KC/16 16-byte
+// segments per thread, staged through registers into LDS rows of KC + 8 bf16.
+template <int KC>
+struct WeightStage {
+  u32x4 v[KC / 16];
+};
+
+template <int KC>
+__device__ inline void load_weights(WeightStage<KC>& w, const uint16_t* __restrict__ tile,
+                                    int64_t ld, int k0) {
+  constexpr int kSegs = KC / 8;
+#pragma unroll
+  for (int j = 0; j < KC / 16; ++j) {
+    const int i = threadIdx.x + kThreads * j;
+    w.v[j] = *reinterpret_cast<const u32x4*>(tile + (int64_t)(i / kSegs) * ld + k0 + 8 * (i % kSegs));
+  }
+}
+
+template <int KC>
+__device__ inline void store_weights(const WeightStage<KC>& w, uint16_t* lds) {
+  constexpr int kSegs = KC / 8;
+#pragma unroll
+  for (int j = 0; j < KC / 16; ++j) {
+    const int i = threadIdx.x + kThreads * j;
+    *reinterpret_cast<u32x4*>(lds + (i / kSegs) * (KC + 8) + 8 * (i % kSegs)) = w.v[j];
+  }
+}
+
+// MFMA work of one stage: the wave's 32 token rows against the 128 weight columns
+// (blocks: gate 0-31, gate 32-63, up 0-31, up 32-63).  ZERO starts the accumulators
+// from zero (first stage of a contraction) instead of adding to them.
+template <int KC, bool ZERO>
+__device__ inline void stage_mfma(const uint16_t* Bs, const TokenFrag<KC>& a, f32x16 (&acc)[4],
+                                  int lane) {
+  const int c = lane & 31;
+  const int off = (lane >> 5) * (KC / 2);
+#pragma unroll
+  for (int s = 0; s < KC / 16; ++s) {
+    const bf16x8 av = __builtin_bit_cast(bf16x8, a.v[s]);
+#pragma unroll
+    for (int b = 0; b < 4; ++b) {
+      const bf16x8 bv =
+          *reinterpret_cast<const bf16x8*>(Bs + (b * 32 + c) * (KC + 8) + off + 8 * s);
+      acc[b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av, bv, (ZERO && s == 0) ? f32x16{} : acc[b],
+                                                       0, 0, 0);
+    }
+  }
+}
+
 // Block = (neuron tile of 64, token split).  For every 128-token tile of its split the
 // block runs one contraction over Kt = d + H*dh in stages of KC:
 //   stages [0, d/KC)          acc = [x] . [W'_gate | W'_up]^T          -> c1, c2 in registers
 //   each next dh/KC stages    acc = [a_h] . [Fg_h | Fu_h]^T            -> Delta^2 column sums
-// Wave w owns token rows 32w..32w+31 and all 128 columns (4 MFMA blocks: gate 0-31,
-// gate 32-63, up 0-31, up 32-63), so c1/c2 and both damage terms of a (token, neuron)
-// pair sit in the same lane.  Column sums are kept per lane over its 16 rows, folded
-// across the two half-waves after the last query head of each KV group, and banked in
-// LDS per (wave, group); the block writes the fixed-order sum over its waves times
-// ||w^d_k||^2 to its split's partial.
+// Wave w owns token rows 32w..32w+31 and all 128 columns, so c1/c2 and both damage terms
+// of a (token, neuron) pair sit in the same lane.  Token operands go from global memory
+// straight to registers one stage ahead; the weight stage is shared by the four waves
+// through a double-buffered LDS tile.  Column sums are kept per lane over its 16 rows,
+// folded across the two half-waves after the last query head of each KV group, and
+// banked in LDS per (wave, group); the block writes the fixed-order sum over its waves
+// times ||w^d_k||^2 to its split's partial.
 template <int KC>
 __global__ void __launch_bounds__(kThreads, 2)
 affinity_bf16_kernel(AffinityArgs p) {
-  constexpr int kRow = KC + 8;
-  __shared__ __attribute__((aligned(16))) uint16_t As[2][kBM * kRow];
-  __shared__ __attribute__((aligned(16))) uint16_t Bs[2][kCols * kRow];
+  __shared__ __attribute__((aligned(16))) uint16_t Bs[2][kCols * (KC + 8)];
   extern __shared__ float red[];  // [kWaves][G][kBN]
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int tile = blockIdx.x / p.splits;
@@ -314,35 +379,37 @@ affinity_bf16_kernel(AffinityArgs p) {
 
   for (int mt = mt_begin; mt < mt_end; ++mt) {
     const int m0 = mt * kBM;
-    const int rows_valid = min(kBM, p.T - m0);
-    const uint16_t* x_tile = p.x + (int64_t)m0 * p.d;
-    const uint16_t* a_tile = p.attn + (int64_t)m0 * HD;
-    auto load = [&](int q, Stage<KC>& sa, Stage<KC>& sb) {
-      const int k0 = q * KC;
-      if (q < nq1)
-        stage_load<KC>(sa, x_tile, p.d, rows_valid, k0, p.d);
-      else
-        stage_load<KC>(sa, a_tile, HD, rows_valid, k0 - p.d, HD);
-      stage_load<KC>(sb, w_tile, p.Kt, kCols, k0, p.Kt);
-    };
+    const int my_row = m0 + wave * 32 + (lane & 31);
+    const bool row_ok = my_row < p.T;
+    const int64_t safe_row = row_ok ? my_row : 0;
+    const uint16_t* xrow = p.x + safe_row * p.d + (lane >> 5) * (KC / 2);
+    const uint16_t* arow = p.attn + safe_row * HD + (lane >> 5) * (KC / 2) - p.d;
 
     f32x16 acc[4];
-#pragma unroll
-    for (int b = 0; b < 4; ++b) acc[b] = f32x16{};
     float c1[2][16], c2[2][16];
     float colsum[2] = {0.0f, 0.0f};
-
-    Stage<KC> sa, sb;
-    load(0, sa, sb);
-    stage_store<KC>(sa, As[0]);
-    stage_store<KC>(sb, Bs[0]);
-    __syncthreads();
     int head_stage = 0;  // stages done of the current head
     int h = 0;
-    for (int q = 0; q < nq; ++q) {
+    TokenFrag<KC> ta, tb;
+    WeightStage<KC> ws;
+    load_tokens<KC>(ta, xrow, row_ok);
+    load_weights<KC>(ws, w_tile, p.Kt, 0);
+    store_weights<KC>(ws, Bs[0]);
+    __syncthreads();
+
+    // One stage q with the tokens in `cur`; prefetches stage q + 1 into `nxt`.
+    auto stage = [&](int q, TokenFrag<KC>& cur, TokenFrag<KC>& nxt) {
       const int buf = q & 1;
-      if (q + 1 < nq) load(q + 1, sa, sb);
-      mfma_stage<KC>(As[buf], Bs[buf], acc, wave, lane);
+      const bool more = q + 1 < nq;
+      if (more) {
+        const int k1 = (q + 1) * KC;
+        load_tokens<KC>(nxt, (q + 1 < nq1 ? xrow : arow) + k1, row_ok);
+        load_weights<KC>(ws, w_tile, p.Kt, k1);
+      }
+      if (q == 0 || (q >= nq1 && head_stage == 0))
+        stage_mfma<KC, true>(Bs[buf], cur, acc, lane);
+      else
+        stage_mfma<KC, false>(Bs[buf], cur, acc, lane);
       if (q == nq1 - 1) {
         // Operating point: g, u -> c1 = silu'(g) u / r, c2 = silu(g) / r.
 #pragma unroll
@@ -358,8 +425,6 @@ affinity_bf16_kernel(AffinityArgs p) {
             c1[j][i] = sg * (1.0f + g * (1.0f - sg)) * u * ri;
           }
         }
-#pragma unroll
-        for (int b = 0; b < 4; ++b) acc[b] = f32x16{};
       } else if (q >= nq1 && ++head_stage == nqh) {
         // Head h done: Delta = c1 (a_h . Fg) + c2 (a_h . Fu); sum Delta^2 over the rows.
 #pragma unroll
@@ -369,8 +434,6 @@ affinity_bf16_kernel(AffinityArgs p) {
             const float dl = c1[j][i] * acc[j][i] + c2[j][i] * acc[2 + j][i];
             colsum[j] = fmaf(dl, dl, colsum[j]);
           }
-#pragma unroll
-        for (int b = 0; b < 4; ++b) acc[b] = f32x16{};
         head_stage = 0;
         if (h % hpg == hpg - 1) {
           // Last query head of its KV group: fold the two half-waves and bank the sums.
@@ -381,12 +444,17 @@ affinity_bf16_kernel(AffinityArgs p) {
         }
         ++h;
       }
-      if (q + 1 < nq) {
-        stage_store<KC>(sa, As[buf ^ 1]);
-        stage_store<KC>(sb, Bs[buf ^ 1]);
-      }
+      if (more) store_weights<KC>(ws, Bs[buf ^ 1]);
       __syncthreads();
+    };
+
+    // Unrolled by two so the token registers alternate without copies.
+    int q = 0;
+    for (; q + 1 < nq; q += 2) {
+      stage(q, ta, tb);
+      stage(q + 1, tb, ta);
     }
+    if (q < nq) stage(q, ta, tb);
   }
 
   // Sum the waves in a fixed order and scale by ||w^d_k||^2.
@@ -687,7 +755,10 @@ dtp_status dtp_affinity_accumulate(dtp_layer L, const void* x, const void* attn,
       p.I_pad = L->I_pad;
       p.Kt = L->Kt;
       const size_t shm = sizeof(float) * kWaves * G * kBN;
-      affinity_bf16_kernel<16><<<L->n_tiles * splits, kThreads, shm, s>>>(p);
+      if (dm % 32 == 0 && dh % 32 == 0)
+        affinity_bf16_kernel<32><<<L->n_tiles * splits, kThreads, shm, s>>>(p);
+      else
+        affinity_bf16_kernel<16><<<L->n_tiles * splits, kThreads, shm, s>>>(p);
     } else {
       splits = (kTargetBlocks / 4 + L->n_tiles - 1) / L->n_tiles;
       splits = std::max(1, std::min(splits, std::min(T, kMaxSplits)));
