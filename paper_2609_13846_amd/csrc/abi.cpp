@@ -271,14 +271,15 @@ dtp_status dtp_coordinate_ascent(int32_t N, int32_t G, int32_t I, int32_t L, con
     ScoreWorkspace* w;
     ~WsGuard() { score_workspace_destroy(w); }
   } guard{&ws};
-  DevBuf qu_dev, qd_dev, nu_dev;
-  DTP_HIP(hipMalloc(&qu_dev.p, sizeof(int64_t) * nup));
-  DTP_HIP(hipMalloc(&nu_dev.p, sizeof(int32_t) * (size_t)N * I));
-  DTP_HIP(hipMemcpyAsync(qu_dev.p, Qu.data(), sizeof(int64_t) * nup, hipMemcpyHostToDevice, s));
-  if (has_down) {
-    DTP_HIP(hipMalloc(&qd_dev.p, sizeof(int64_t) * ndown));
-    DTP_HIP(hipMemcpyAsync(qd_dev.p, Qd.data(), sizeof(int64_t) * ndown, hipMemcpyHostToDevice, s));
-  }
+  // One device block for the codes and the neuron assignments: [Q_up | Q_down | nu].
+  DevBuf block;
+  const size_t qu_bytes = sizeof(int64_t) * nup, qd_bytes = sizeof(int64_t) * ndown;
+  DTP_HIP(hipMalloc(&block.p, qu_bytes + qd_bytes + sizeof(int32_t) * (size_t)N * I));
+  int64_t* qu_dev = (int64_t*)block.p;
+  int64_t* qd_dev = has_down ? qu_dev + nup : nullptr;
+  int32_t* nu_dev = (int32_t*)((char*)block.p + qu_bytes + qd_bytes);
+  DTP_HIP(hipMemcpyAsync(qu_dev, Qu.data(), qu_bytes, hipMemcpyHostToDevice, s));
+  if (has_down) DTP_HIP(hipMemcpyAsync(qd_dev, Qd.data(), qd_bytes, hipMemcpyHostToDevice, s));
   const std::vector<uint8_t> table = enumerate_partitions(G, L);
 
   // Contiguous start.
@@ -298,28 +299,29 @@ dtp_status dtp_coordinate_ascent(int32_t N, int32_t G, int32_t I, int32_t L, con
       // Neuron block: layers are independent given the heads; solve them in parallel.
       const unsigned hw = std::max(1u, std::thread::hardware_concurrency());
       const int nthreads = (int)std::min<unsigned>(hw, (unsigned)N);
-      std::vector<std::thread> pool;
-      for (int t = 0; t < nthreads; ++t) {
-        pool.emplace_back([&, t]() {
-          std::vector<int64_t> M;
-          for (int i = t; i < N; i += nthreads) {
-            if (!moves(i)) continue;
-            const bool dn = has_down && i + 1 < N;
-            neuron_gain(G, I, L, Qu.data() + (size_t)i * G * I, hs.data() + (size_t)i * G,
-                        dn ? Qd.data() + (size_t)i * I * G : nullptr,
-                        dn ? hs.data() + (size_t)(i + 1) * G : nullptr, minimise, &M);
-            balanced_assign_exact(I, L, M.data(), nus.data() + (size_t)i * I, nullptr);
-          }
-        });
+      auto work = [&](int t) {
+        std::vector<int64_t> M;
+        for (int i = t; i < N; i += nthreads) {
+          if (!moves(i)) continue;
+          const bool dn = has_down && i + 1 < N;
+          neuron_gain(G, I, L, Qu.data() + (size_t)i * G * I, hs.data() + (size_t)i * G,
+                      dn ? Qd.data() + (size_t)i * I * G : nullptr,
+                      dn ? hs.data() + (size_t)(i + 1) * G : nullptr, minimise, &M);
+          balanced_assign_exact(I, L, M.data(), nus.data() + (size_t)i * I, nullptr);
+        }
+      };
+      if (nthreads == 1) {
+        work(0);
+      } else {
+        std::vector<std::thread> pool;
+        for (int t = 0; t < nthreads; ++t) pool.emplace_back(work, t);
+        for (auto& th : pool) th.join();
       }
-      for (auto& th : pool) th.join();
     }
     if (!opt.freeze_heads) {
-      DTP_HIP(hipMemcpyAsync(nu_dev.p, nus.data(), sizeof(int32_t) * (size_t)N * I,
+      DTP_HIP(hipMemcpyAsync(nu_dev, nus.data(), sizeof(int32_t) * (size_t)N * I,
                              hipMemcpyHostToDevice, s));
-      st = launch_partition_scores(ws, (const int64_t*)qu_dev.p, (const int32_t*)nu_dev.p,
-                                   (const int64_t*)qd_dev.p, (const int32_t*)nu_dev.p,
-                                   minimise ? 1 : 0, s);
+      st = launch_partition_scores(ws, qu_dev, nu_dev, qd_dev, nu_dev, minimise ? 1 : 0, s);
       if (st != DTP_OK) return st;
       DTP_HIP(hipMemcpyAsync(best.data(), ws.best, sizeof(int64_t) * N, hipMemcpyDeviceToHost, s));
       DTP_HIP(hipStreamSynchronize(s));

@@ -47,7 +47,6 @@ constexpr int kCols = 2 * kBN;    // MFMA columns per tile: 64 gate | 64 up
 constexpr int kKC = 32;           // contraction depth per LDS stage of the fold
 constexpr int kLdsRow = kKC + 8;  // bf16 per LDS row
 constexpr int kThreads = 256;
-constexpr int kWaves = kThreads / 64;
 constexpr int kSliceTokens = 1 << 18;  // tokens per internal slice (size of the 1/r buffer)
 constexpr int kMaxSplits = 128;        // token splits per launch (size of the partials)
 constexpr int kTargetBlocks = 3072;    // aim for this many blocks per launch
@@ -234,18 +233,27 @@ __global__ void fold_f32_kernel(const float* __restrict__ w_o, const float* __re
   }
 }
 
+// nd[k] = sum_j w_down[j][k]^2.  Block = 64 columns x 16 row groups; the row groups'
+// partial sums are added in a fixed order.
 template <typename T>
-__global__ void down_norm_kernel(const T* __restrict__ w_down, int d, int I, int I_pad,
-                                 float* __restrict__ nd) {
-  const int k = blockIdx.x * blockDim.x + threadIdx.x;
-  if (k >= I_pad) return;
+__global__ void __launch_bounds__(1024)
+down_norm_kernel(const T* __restrict__ w_down, int d, int I, int I_pad, float* __restrict__ nd) {
+  __shared__ float part[16][64];
+  const int c = threadIdx.x & 63, rg = threadIdx.x >> 6;
+  const int k = blockIdx.x * 64 + c;
   float s = 0.0f;
   if (k < I)
-    for (int j = 0; j < d; ++j) {
+    for (int j = rg; j < d; j += 16) {
       const float v = load_f32(w_down, (int64_t)j * I + k);
       s = fmaf(v, v, s);
     }
-  nd[k] = s;
+  part[rg][c] = s;
+  __syncthreads();
+  if (rg == 0 && k < I_pad) {
+    float t = 0.0f;
+    for (int r = 0; r < 16; ++r) t += part[r][c];
+    nd[k] = t;
+  }
 }
 
 // ------------------------------------------------------------------ per-token scalars
@@ -258,9 +266,22 @@ rms_kernel(const T* __restrict__ x, int64_t T_tokens, int d, float eps, float* _
   if (t >= T_tokens) return;  // whole wavefronts exit together
   const T* row = x + t * d;
   float s = 0.0f;
-  for (int j = lane; j < d; j += 64) {
-    const float v = load_f32(row, j);
-    s = fmaf(v, v, s);
+  if constexpr (sizeof(T) == 2) {
+    // d % 16 == 0: 16-byte loads of 8 bf16
+    for (int j = lane * 8; j < d; j += 64 * 8) {
+      const u32x4 v = *reinterpret_cast<const u32x4*>(row + j);
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const float lo = __uint_as_float(v[e] << 16), hi = __uint_as_float(v[e] & 0xffff0000u);
+        s = fmaf(lo, lo, s);
+        s = fmaf(hi, hi, s);
+      }
+    }
+  } else {
+    for (int j = lane; j < d; j += 64) {
+      const float v = load_f32(row, j);
+      s = fmaf(v, v, s);
+    }
   }
   for (int off = 32; off > 0; off >>= 1) s += __shfl_xor(s, off, 64);
   if (lane == 0) rinv[t] = 1.0f / sqrtf(s / (float)d + eps);
@@ -288,43 +309,46 @@ struct TokenFrag {
 };
 
 template <int KC>
-__device__ inline void load_tokens(TokenFrag<KC>& f, const uint16_t* __restrict__ src, bool valid) {
+__device__ inline void load_tokens(TokenFrag<KC>& f, const uint16_t* __restrict__ src) {
 #pragma unroll
-  for (int s = 0; s < KC / 16; ++s)
-    f.v[s] = valid ? *reinterpret_cast<const u32x4*>(src + 8 * s) : u32x4{0u, 0u, 0u, 0u};
+  for (int s = 0; s < KC / 16; ++s) f.v[s] = *reinterpret_cast<const u32x4*>(src + 8 * s);
 }
 
-// A stage of the weight tile: 128 columns x KC contraction elements, KC/16 16-byte
-// segments per thread, staged through registers into LDS rows of KC + 8 bf16.
-template <int KC>
+// A stage of a block's weight tile: COLS columns x KC contraction elements spread over
+// NT threads (KC*COLS/(8*NT) 16-byte segments each), staged through registers into LDS rows
+// of KC + 8 bf16 (the 16 bytes of padding spread consecutive rows over the banks).
+template <int KC, int COLS, int NT>
 struct WeightStage {
-  u32x4 v[KC / 16];
+  static constexpr int kSegs = KC / 8;                  // per column
+  static constexpr int kPerThread = COLS * kSegs / NT;  // per thread
+  static_assert(kPerThread >= 1 && COLS * kSegs % NT == 0, "stage does not split evenly");
+  u32x4 v[kPerThread];
 };
 
-template <int KC>
-__device__ inline void load_weights(WeightStage<KC>& w, const uint16_t* __restrict__ tile,
+template <int KC, int COLS, int NT>
+__device__ inline void load_weights(WeightStage<KC, COLS, NT>& w, const uint16_t* __restrict__ tile,
                                     int64_t ld, int k0) {
-  constexpr int kSegs = KC / 8;
+  constexpr int kSegs = WeightStage<KC, COLS, NT>::kSegs;
 #pragma unroll
-  for (int j = 0; j < KC / 16; ++j) {
-    const int i = threadIdx.x + kThreads * j;
+  for (int j = 0; j < WeightStage<KC, COLS, NT>::kPerThread; ++j) {
+    const int i = threadIdx.x + NT * j;
     w.v[j] = *reinterpret_cast<const u32x4*>(tile + (int64_t)(i / kSegs) * ld + k0 + 8 * (i % kSegs));
   }
 }
 
-template <int KC>
-__device__ inline void store_weights(const WeightStage<KC>& w, uint16_t* lds) {
-  constexpr int kSegs = KC / 8;
+template <int KC, int COLS, int NT>
+__device__ inline void store_weights(const WeightStage<KC, COLS, NT>& w, uint16_t* lds) {
+  constexpr int kSegs = WeightStage<KC, COLS, NT>::kSegs;
 #pragma unroll
-  for (int j = 0; j < KC / 16; ++j) {
-    const int i = threadIdx.x + kThreads * j;
+  for (int j = 0; j < WeightStage<KC, COLS, NT>::kPerThread; ++j) {
+    const int i = threadIdx.x + NT * j;
     *reinterpret_cast<u32x4*>(lds + (i / kSegs) * (KC + 8) + 8 * (i % kSegs)) = w.v[j];
   }
 }
 
-// MFMA work of one stage: the wave's 32 token rows against the 128 weight columns
-// (blocks: gate 0-31, gate 32-63, up 0-31, up 32-63).  ZERO starts the accumulators
-// from zero (first stage of a contraction) instead of adding to them.
+// MFMA work of one stage: the wave's 32 token rows against its 128 weight columns
+// (blocks: gate 0-31, gate 32-63, up 0-31, up 32-63 of its 64 neurons).  ZERO starts the
+// accumulators from zero (first stage of a contraction) instead of adding to them.
 template <int KC, bool ZERO>
 __device__ inline void stage_mfma(const uint16_t* Bs, const TokenFrag<KC>& a, f32x16 (&acc)[4],
                                   int lane) {
@@ -343,84 +367,96 @@ __device__ inline void stage_mfma(const uint16_t* Bs, const TokenFrag<KC>& a, f3
   }
 }
 
-// Block = (neuron tile of 64, token split).  For every 128-token tile of its split the
-// block runs one contraction over Kt = d + H*dh in stages of KC:
+// Block = (WN neuron tiles of 64, token split), WM x WN wavefronts.  For every tile of
+// 32*WM tokens of its split the block runs one contraction over Kt = d + H*dh in stages
+// of KC:
 //   stages [0, d/KC)          acc = [x] . [W'_gate | W'_up]^T          -> c1, c2 in registers
 //   each next dh/KC stages    acc = [a_h] . [Fg_h | Fu_h]^T            -> Delta^2 column sums
-// Wave w owns token rows 32w..32w+31 and all 128 columns, so c1/c2 and both damage terms
-// of a (token, neuron) pair sit in the same lane.  Token operands go from global memory
-// straight to registers one stage ahead; the weight stage is shared by the four waves
-// through a double-buffered LDS tile.  Column sums are kept per lane over its 16 rows,
-// folded across the two half-waves after the last query head of each KV group, and
-// banked in LDS per (wave, group); the block writes the fixed-order sum over its waves
+// Wave (wm, wn) owns token rows 32wm..32wm+31 and the 128 columns of neuron tile wn, so
+// c1/c2 and both damage terms of a (token, neuron) pair sit in the same lane.  Both
+// operands are fetched two stages ahead into registers: the token rows go straight to
+// the MFMAs, the weight stage shared by the block is written to a double-buffered LDS
+// tile one stage before use.  Rows past the last token are clamped to a real row and
+// given zero coefficients.  Column sums are kept per lane over its 16 rows, folded
+// across the two half-waves after the last query head of each KV group, and banked in
+// LDS per (wave, group); the block writes the fixed-order sum over its WM row waves
 // times ||w^d_k||^2 to its split's partial.
-template <int KC>
-__global__ void __launch_bounds__(kThreads, 2)
+template <int KC, int WM, int WN>
+__global__ void __launch_bounds__(64 * WM * WN, 8 / (WM * WN))
 affinity_bf16_kernel(AffinityArgs p) {
-  __shared__ __attribute__((aligned(16))) uint16_t Bs[2][kCols * (KC + 8)];
-  extern __shared__ float red[];  // [kWaves][G][kBN]
+  constexpr int NT = 64 * WM * WN;
+  constexpr int kRows = 32 * WM;
+  constexpr int kStageCols = kCols * WN;
+  using WStage = WeightStage<KC, kStageCols, NT>;
+  __shared__ __attribute__((aligned(16))) uint16_t Bs[2][kStageCols * (KC + 8)];
+  extern __shared__ float red[];  // [WM*WN][G][kBN]
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
-  const int tile = blockIdx.x / p.splits;
+  const int wm = wave % WM, wn = wave / WM;
+  const int tg = blockIdx.x / p.splits;  // group of WN neuron tiles
   const int split = blockIdx.x % p.splits;
   const int HD = p.H * p.dh;
   const int hpg = p.H / p.G;
 
-  for (int i = threadIdx.x; i < kWaves * p.G * kBN; i += kThreads) red[i] = 0.0f;
+  for (int i = threadIdx.x; i < WM * WN * p.G * kBN; i += NT) red[i] = 0.0f;
 
-  const int mtiles = (p.T + kBM - 1) / kBM;
+  const int mtiles = (p.T + kRows - 1) / kRows;
   const int per = (mtiles + p.splits - 1) / p.splits;
   const int mt_begin = split * per;
   const int mt_end = min(mtiles, mt_begin + per);
   const int nq1 = p.d / KC;   // operating-point stages
   const int nqh = p.dh / KC;  // stages per head
   const int nq = nq1 + p.H * nqh;
-  const uint16_t* w_tile = p.wcat + (int64_t)tile * kCols * p.Kt;
+  const uint16_t* w_tile = p.wcat + (int64_t)tg * kStageCols * p.Kt;
+  const int bs_off = wn * kCols * (KC + 8);  // this wave's columns inside the LDS stage
   __syncthreads();
 
   for (int mt = mt_begin; mt < mt_end; ++mt) {
-    const int m0 = mt * kBM;
-    const int my_row = m0 + wave * 32 + (lane & 31);
-    const bool row_ok = my_row < p.T;
-    const int64_t safe_row = row_ok ? my_row : 0;
-    const uint16_t* xrow = p.x + safe_row * p.d + (lane >> 5) * (KC / 2);
-    const uint16_t* arow = p.attn + safe_row * HD + (lane >> 5) * (KC / 2) - p.d;
+    const int m0 = mt * kRows;
+    const int64_t row = min(m0 + wm * 32 + (lane & 31), p.T - 1);
+    const uint16_t* xrow = p.x + row * p.d + (lane >> 5) * (KC / 2);
+    const uint16_t* arow = p.attn + row * HD + (lane >> 5) * (KC / 2) - p.d;
+    auto token_src = [&](int q) { return (q < nq1 ? xrow : arow) + q * KC; };
 
     f32x16 acc[4];
     float c1[2][16], c2[2][16];
     float colsum[2] = {0.0f, 0.0f};
     int head_stage = 0;  // stages done of the current head
     int h = 0;
-    TokenFrag<KC> ta, tb;
-    WeightStage<KC> ws;
-    load_tokens<KC>(ta, xrow, row_ok);
-    load_weights<KC>(ws, w_tile, p.Kt, 0);
-    store_weights<KC>(ws, Bs[0]);
+    TokenFrag<KC> t0, t1, t2;
+    WStage w0, w1;
+    load_tokens<KC>(t0, token_src(0));
+    load_weights(w0, w_tile, p.Kt, 0);
+    if (nq > 1) {
+      load_tokens<KC>(t1, token_src(1));
+      load_weights(w1, w_tile, p.Kt, KC);
+    }
+    store_weights(w0, Bs[0]);
     __syncthreads();
 
-    // One stage q with the tokens in `cur`; prefetches stage q + 1 into `nxt`.
-    auto stage = [&](int q, TokenFrag<KC>& cur, TokenFrag<KC>& nxt) {
+    // Stage q: tokens in `cur`, stage q+1's weights in `wnext` (stored to LDS here),
+    // stage q+2 fetched into `tnew` / `wnew`.
+    auto stage = [&](int q, TokenFrag<KC>& cur, TokenFrag<KC>& tnew, WStage& wnext,
+                     WStage& wnew) {
       const int buf = q & 1;
-      const bool more = q + 1 < nq;
-      if (more) {
-        const int k1 = (q + 1) * KC;
-        load_tokens<KC>(nxt, (q + 1 < nq1 ? xrow : arow) + k1, row_ok);
-        load_weights<KC>(ws, w_tile, p.Kt, k1);
+      if (q + 2 < nq) {
+        load_tokens<KC>(tnew, token_src(q + 2));
+        load_weights(wnew, w_tile, p.Kt, (q + 2) * KC);
       }
       if (q == 0 || (q >= nq1 && head_stage == 0))
-        stage_mfma<KC, true>(Bs[buf], cur, acc, lane);
+        stage_mfma<KC, true>(Bs[buf] + bs_off, cur, acc, lane);
       else
-        stage_mfma<KC, false>(Bs[buf], cur, acc, lane);
+        stage_mfma<KC, false>(Bs[buf] + bs_off, cur, acc, lane);
       if (q == nq1 - 1) {
         // Operating point: g, u -> c1 = silu'(g) u / r, c2 = silu(g) / r.
 #pragma unroll
         for (int i = 0; i < 16; ++i) {
-          const int row = m0 + wave * 32 + acc_row(i, lane);
-          const float ri = row < p.T ? p.rinv[row] : 0.0f;
+          const int r = m0 + wm * 32 + acc_row(i, lane);
+          const float ri = r < p.T ? p.rinv[r] : 0.0f;
 #pragma unroll
           for (int j = 0; j < 2; ++j) {
             const float g = acc[j][i] * ri;
             const float u = acc[2 + j][i] * ri;
-            const float sg = 1.0f / (1.0f + __expf(-g));
+            const float sg = __builtin_amdgcn_rcpf(1.0f + __expf(-g));
             c2[j][i] = g * sg * ri;
             c1[j][i] = sg * (1.0f + g * (1.0f - sg)) * u * ri;
           }
@@ -444,27 +480,47 @@ affinity_bf16_kernel(AffinityArgs p) {
         }
         ++h;
       }
-      if (more) store_weights<KC>(ws, Bs[buf ^ 1]);
+      if (q + 1 < nq) store_weights(wnext, Bs[buf ^ 1]);
       __syncthreads();
     };
 
-    // Unrolled by two so the token registers alternate without copies.
+    // Unrolled by six so the three token and two weight register sets rotate in place.
     int q = 0;
-    for (; q + 1 < nq; q += 2) {
-      stage(q, ta, tb);
-      stage(q + 1, tb, ta);
+    for (; q + 5 < nq; q += 6) {
+      stage(q, t0, t2, w1, w0);
+      stage(q + 1, t1, t0, w0, w1);
+      stage(q + 2, t2, t1, w1, w0);
+      stage(q + 3, t0, t2, w0, w1);
+      stage(q + 4, t1, t0, w1, w0);
+      stage(q + 5, t2, t1, w0, w1);
     }
-    if (q < nq) stage(q, ta, tb);
+    if (q < nq) stage(q, t0, t2, w1, w0);
+    if (q + 1 < nq) stage(q + 1, t1, t0, w0, w1);
+    if (q + 2 < nq) stage(q + 2, t2, t1, w1, w0);
+    if (q + 3 < nq) stage(q + 3, t0, t2, w0, w1);
+    if (q + 4 < nq) stage(q + 4, t1, t0, w1, w0);
   }
 
-  // Sum the waves in a fixed order and scale by ||w^d_k||^2.
-  for (int i = threadIdx.x; i < p.G * kBN; i += kThreads) {
-    const int g = i / kBN, k = i % kBN;
+  // Sum the row waves in a fixed order and scale by ||w^d_k||^2.
+  for (int i = threadIdx.x; i < p.G * kBN * WN; i += NT) {
+    const int g = i / (kBN * WN), nl = i % (kBN * WN);
+    const int cw = nl / kBN, k = nl % kBN;
     float s = 0.0f;
-    for (int w = 0; w < kWaves; ++w) s += red[(w * p.G + g) * kBN + k];
-    const int n = tile * kBN + k;
+    for (int w = 0; w < WM; ++w) s += red[((cw * WM + w) * p.G + g) * kBN + k];
+    const int n = tg * kBN * WN + nl;
     p.partial[((int64_t)split * p.G + g) * p.I_pad + n] = s * p.nd[n];
   }
+}
+
+// Launch shape of the bf16 affinity kernel for one slice of T tokens.
+struct AffinityLaunch {
+  int kc, wm, wn;
+};
+
+template <int KC, int WM, int WN>
+void launch_affinity(const AffinityArgs& p, int n_tiles, hipStream_t s) {
+  const size_t shm = sizeof(float) * WM * WN * p.G * kBN;
+  affinity_bf16_kernel<KC, WM, WN><<<(n_tiles / WN) * p.splits, 64 * WM * WN, shm, s>>>(p);
 }
 
 // ------------------------------------------------------------------ fused affinity (fp32)
@@ -622,7 +678,7 @@ dtp_status dtp_layer_create(const dtp_layer_desc* desc, dtp_layer* out) {
   DTP_CHECK(L != nullptr, DTP_ERR_NO_MEMORY, "host allocation failed");
   L->desc = d;
   hipError_t e = hipGetDevice(&L->device);
-  L->n_tiles = (d.n_neurons + kBN - 1) / kBN;
+  L->n_tiles = (d.n_neurons + 2 * kBN - 1) / (2 * kBN) * 2;  // even: a block may span two tiles
   L->I_pad = L->n_tiles * kBN;
   const int64_t HD = (int64_t)d.n_q_heads * d.head_dim;
   const size_t rows = (size_t)L->n_tiles * kCols;
@@ -678,8 +734,8 @@ dtp_status dtp_layer_set_weights(dtp_layer L, const void* w_o, const void* gamma
     dim3 fg(L->n_tiles * kCols / kBM, (HD + kCols - 1) / kCols);
     fold_kernel<<<fg, kThreads, 0, s>>>((uint16_t*)L->w, (const uint16_t*)L->woT, HD, dm, L->Kt);
     DTP_HIP(hipGetLastError());
-    down_norm_kernel<uint16_t><<<grid_for(L->I_pad, 256), 256, 0, s>>>(
-        (const uint16_t*)w_down, dm, I, L->I_pad, L->nd);
+    down_norm_kernel<uint16_t><<<L->I_pad / 64, 1024, 0, s>>>((const uint16_t*)w_down, dm, I,
+                                                             L->I_pad, L->nd);
     DTP_HIP(hipGetLastError());
   } else {
     prep_gate_up_kernel<float><<<grid_for(n, 256), 256, 0, s>>>(
@@ -691,8 +747,8 @@ dtp_status dtp_layer_set_weights(dtp_layer L, const void* w_o, const void* gamma
                                                        (const float*)w_gate, (const float*)w_up,
                                                        dm, I, H, dh, L->fold32);
     DTP_HIP(hipGetLastError());
-    down_norm_kernel<float><<<grid_for(L->I_pad, 256), 256, 0, s>>>((const float*)w_down, dm, I,
-                                                                     L->I_pad, L->nd);
+    down_norm_kernel<float><<<L->I_pad / 64, 1024, 0, s>>>((const float*)w_down, dm, I, L->I_pad,
+                                                           L->nd);
     DTP_HIP(hipGetLastError());
   }
   L->has_weights = true;
@@ -735,9 +791,6 @@ dtp_status dtp_affinity_accumulate(dtp_layer L, const void* x, const void* attn,
       DTP_HIP(hipEventRecord(e0, s));
     }
     if (d.dtype == DTP_BF16) {
-      const int mtiles = (T + kBM - 1) / kBM;
-      splits = (kTargetBlocks + L->n_tiles - 1) / L->n_tiles;
-      splits = std::max(1, std::min(splits, std::min(mtiles, kMaxSplits)));
       AffinityArgs p;
       p.x = (const uint16_t*)xs;
       p.attn = (const uint16_t*)as;
@@ -751,14 +804,18 @@ dtp_status dtp_affinity_accumulate(dtp_layer L, const void* x, const void* attn,
       p.G = G;
       p.dh = dh;
       p.n_tiles = L->n_tiles;
-      p.splits = splits;
       p.I_pad = L->I_pad;
       p.Kt = L->Kt;
-      const size_t shm = sizeof(float) * kWaves * G * kBN;
-      if (dm % 32 == 0 && dh % 32 == 0)
-        affinity_bf16_kernel<32><<<L->n_tiles * splits, kThreads, shm, s>>>(p);
+      const bool kc32 = dm % 32 == 0 && dh % 32 == 0;
+      const int rows = 128;  // 32 * WM
+      const int mtiles = (T + rows - 1) / rows;
+      splits = (kTargetBlocks + L->n_tiles - 1) / L->n_tiles;
+      splits = std::max(1, std::min(splits, std::min(mtiles, kMaxSplits)));
+      p.splits = splits;
+      if (kc32)
+        launch_affinity<32, 4, 1>(p, L->n_tiles, s);
       else
-        affinity_bf16_kernel<16><<<L->n_tiles * splits, kThreads, shm, s>>>(p);
+        launch_affinity<16, 4, 1>(p, L->n_tiles, s);
     } else {
       splits = (kTargetBlocks / 4 + L->n_tiles - 1) / L->n_tiles;
       splits = std::max(1, std::min(splits, std::min(T, kMaxSplits)));

@@ -5,7 +5,8 @@
 // replicated slots per device.  The paper solves it approximately (dual ascent, a
 // capacity fix-up, pairwise swaps); this solver is exact.
 //
-// 1. Optimum.  Neurons are inserted one at a time, each along a best augmenting path of
+// 1. Optimum.  With two devices, sorting by M[k][0] - M[k][1] is exact.  Otherwise neurons
+//    are inserted one at a time, each along a best augmenting path of
 //    the current optimal partial assignment (the successive-shortest-path method of the
 //    assignment problem, one row at a time).  Because there are only L devices, a path is
 //    a walk over devices: the new neuron enters device a0, then for every hop a -> b the
@@ -182,6 +183,15 @@ void canonicalise(int I, int L, const int64_t* M, std::vector<int32_t>& nu) {
   }
 }
 
+// Two devices: an optimum puts the I/2 neurons with the largest M[k][0] - M[k][1] on
+// device 0 (exchanging any pair across the cut cannot gain).
+void optimal_two_devices(int I, const int64_t* M, std::vector<int32_t>& nu) {
+  std::vector<std::pair<int64_t, int32_t>> key(I);
+  for (int k = 0; k < I; ++k) key[k] = {M[2 * (size_t)k + 1] - M[2 * (size_t)k], k};
+  std::nth_element(key.begin(), key.begin() + I / 2, key.end());
+  for (int r = 0; r < I; ++r) nu[key[r].second] = r < I / 2 ? 0 : 1;
+}
+
 }  // namespace
 
 void balanced_assign_exact(int I, int L, const int64_t* M, int32_t* nu_out, int64_t* value) {
@@ -189,7 +199,10 @@ void balanced_assign_exact(int I, int L, const int64_t* M, int32_t* nu_out, int6
   if (L == 1) {
     std::fill(nu.begin(), nu.end(), 0);
   } else {
-    optimal_by_insertion(I, L, M, nu);
+    if (L == 2)
+      optimal_two_devices(I, M, nu);
+    else
+      optimal_by_insertion(I, L, M, nu);
     canonicalise(I, L, M, nu);
   }
   int64_t v = 0;

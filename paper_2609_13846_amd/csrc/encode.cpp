@@ -28,16 +28,23 @@ dtp_status encode_unit_mass(const float* A, int64_t n, int64_t* Q) {
   int e = 0;
   std::frexp(amax, &e);  // amax = m * 2^e, m in [0.5, 1)
   const int E = e - 1;   // amax in [2^E, 2^(E+1))
-  const int shift = kMantBits - E;
+  // Scaling an fp32 value by a power of two is exact in fp64 (the product is below 2^41,
+  // and one that underflows truncates to 0 either way); truncation is floor for x >= 0.
+  const double p2 = std::ldexp(1.0, kMantBits - E);
   unsigned __int128 S = 0;
   for (int64_t i = 0; i < n; ++i) {
-    const double q = std::floor(std::ldexp((double)A[i], shift));
-    Q[i] = (int64_t)q;  // temporarily q_i
+    Q[i] = (int64_t)((double)A[i] * p2);  // temporarily q_i
     S += (unsigned __int128)(uint64_t)Q[i];
   }
+  // floor(q * 2^48 / S): a double estimate (within a few units), then an exact integer
+  // correction.
+  const double scale = std::ldexp(1.0, kFracBits) / (double)S;
   for (int64_t i = 0; i < n; ++i) {
     const unsigned __int128 num = (unsigned __int128)(uint64_t)Q[i] << kFracBits;
-    Q[i] = (int64_t)(num / S);
+    uint64_t c = (uint64_t)((double)Q[i] * scale);
+    while ((unsigned __int128)c * S > num) --c;
+    while ((unsigned __int128)(c + 1) * S <= num) ++c;
+    Q[i] = (int64_t)c;
   }
   return DTP_OK;
 }

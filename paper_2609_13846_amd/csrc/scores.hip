@@ -125,19 +125,23 @@ dtp_status score_workspace_create(ScoreWorkspace* ws, int N, int G, int I, int L
             "%lld partitions of %d groups over %d devices exceed the limit of %lld",
             (long long)ws->P, G, L, (long long)kMaxPartitions);
   const std::vector<uint8_t> table = enumerate_partitions(G, L);
-  DTP_HIP(hipMalloc(&ws->table, table.size()));
-  DTP_HIP(hipMalloc(&ws->C, sizeof(int64_t) * (size_t)N * G * L));
-  DTP_HIP(hipMalloc(&ws->scores, sizeof(int64_t) * (size_t)N * ws->P));
-  DTP_HIP(hipMalloc(&ws->best, sizeof(int64_t) * (size_t)N));
+  // One allocation: [C | scores | best | table], each part 256-byte aligned.
+  auto up = [](size_t b) { return (b + 255) & ~size_t(255); };
+  const size_t c_bytes = up(sizeof(int64_t) * (size_t)N * G * L);
+  const size_t s_bytes = up(sizeof(int64_t) * (size_t)N * ws->P);
+  const size_t b_bytes = up(sizeof(int64_t) * (size_t)N);
+  char* base = nullptr;
+  DTP_HIP(hipMalloc(&base, c_bytes + s_bytes + b_bytes + table.size()));
+  ws->C = (int64_t*)base;
+  ws->scores = (int64_t*)(base + c_bytes);
+  ws->best = (int64_t*)(base + c_bytes + s_bytes);
+  ws->table = (uint8_t*)(base + c_bytes + s_bytes + b_bytes);
   DTP_HIP(hipMemcpy(ws->table, table.data(), table.size(), hipMemcpyHostToDevice));
   return DTP_OK;
 }
 
 void score_workspace_destroy(ScoreWorkspace* ws) {
-  if (ws->table) (void)hipFree(ws->table);
   if (ws->C) (void)hipFree(ws->C);
-  if (ws->scores) (void)hipFree(ws->scores);
-  if (ws->best) (void)hipFree(ws->best);
   *ws = ScoreWorkspace();
 }
 
