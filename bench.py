@@ -198,7 +198,10 @@ def main():
     dtp.dtp_layer_profile(layer, 0)
     ms_per_step = (t1 - t0) * 1e3 / args.steps
     value = T / (ms_per_step * 1e-3)
-    f_launch = flops_per_token(wl) * T
+    # The library splits a call into slices, one kernel launch each: the algorithmic work
+    # of a launch is the FLOPs of the tokens it covers.
+    launches_per_step = launches / max(args.steps, 1)
+    f_launch = flops_per_token(wl) * T / max(launches_per_step, 1)
     avg_ms = kern_ms / max(launches, 1)
     achieved = f_launch / (avg_ms * 1e-3) / 1e12
     traffic = traffic_record(wl)
@@ -222,8 +225,9 @@ def main():
                      "achieved": achieved, "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
                      "frac": achieved / PEAK_BF16_TFLOPS, "traffic": traffic,
                      "avg_launch_ms": avg_ms, "launches": launches,
+                     "tokens_per_launch": T / max(launches_per_step, 1),
                      "flops_per_launch": f_launch},
-        "step_tflops": f_launch / (ms_per_step * 1e-3) / 1e12,
+        "step_tflops": flops_per_token(wl) * T / (ms_per_step * 1e-3) / 1e12,
         "breakdown_ms": {"fold": (b1 - b0) * 1e3, "affinity": (b2 - b1) * 1e3,
                          "layout": (b3 - b2) * 1e3},
         "layout": {"J": res["J"], "sweeps": res["sweeps"]},

@@ -49,6 +49,7 @@ constexpr int kLdsRow = kKC + 8;  // bf16 per LDS row
 constexpr int kThreads = 256;
 constexpr int kSliceTokens = 1 << 18;  // tokens per internal slice (size of the 1/r buffer)
 constexpr int kMaxSplits = 128;        // token splits per launch (size of the partials)
+constexpr int kTileTokens = 1 << 15;   // tokens per bf16 slice (size of the tiled token buffer)
 constexpr int kTargetBlocks = 3072;    // aim for this many blocks per launch
 
 __device__ inline float bf16_to_f32(uint16_t b) { return __uint_as_float((uint32_t)b << 16); }
@@ -287,32 +288,47 @@ rms_kernel(const T* __restrict__ x, int64_t T_tokens, int d, float eps, float* _
   if (lane == 0) rinv[t] = 1.0f / sqrtf(s / (float)d + eps);
 }
 
+// ------------------------------------------------------------------ token tiling (bf16)
+// The MFMA operand layout gives lane l token row l % 32, so a wavefront reading its
+// fragments straight from row-major [T][d] rows touches 32 rows per load, which the
+// vector memory path serves at a quarter of its rate for contiguous loads.  Each slice of
+// tokens is therefore first rewritten so that every fragment is one contiguous 1 KB run:
+//   xt[rb][q][s][h][r][e] = [x | attn][32*rb + r][q*KC + h*KC/2 + 8*s + e]
+// for 32-row block rb, stage q of KC columns, k-step s < KC/16, half h, row r < 32 and
+// element e < 8 (rows past the last token are zero).  One thread moves one 16-byte chunk;
+// consecutive threads read consecutive chunks of a row.
+template <int KC>
+__global__ void __launch_bounds__(256)
+tile_tokens_kernel(const uint16_t* __restrict__ x, const uint16_t* __restrict__ attn, int T, int d,
+                   int HD, int nq, int64_t n_chunks, uint16_t* __restrict__ xt) {
+  constexpr int kRowChunks = KC / 8;
+  constexpr int kUnitChunks = 32 * kRowChunks;
+  const int64_t g = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (g >= n_chunks) return;
+  const int64_t u = g / kUnitChunks;  // (row block, stage)
+  const int w = (int)(g % kUnitChunks);
+  const int r = w / kRowChunks, c = w % kRowChunks;
+  const int64_t rb = u / nq;
+  const int q = (int)(u % nq);
+  const int64_t t = 32 * rb + r;
+  const int k0 = q * KC + 8 * c;
+  u32x4 v = {0u, 0u, 0u, 0u};
+  if (t < T)
+    v = k0 < d ? *reinterpret_cast<const u32x4*>(x + t * d + k0)
+               : *reinterpret_cast<const u32x4*>(attn + t * HD + (k0 - d));
+  const int h = c / (KC / 16), s = c % (KC / 16);
+  *reinterpret_cast<u32x4*>(xt + u * (32 * KC) + ((s * 2 + h) * 32 + r) * 8) = v;
+}
+
 // ------------------------------------------------------------------ fused affinity (bf16)
 struct AffinityArgs {
-  const uint16_t* x;      // [T][d]
-  const uint16_t* attn;   // [T][H*dh]
+  const uint16_t* xt;     // token rows [x | attn] in the tiled layout of tile_tokens_kernel
   const uint16_t* wcat;   // [n_tiles*128][Kt], Kt = d + H*dh
   const float* rinv;      // [T]
   const float* nd;        // [I_pad]
   float* partial;         // [splits][G][I_pad]
-  int T, d, H, G, dh, n_tiles, splits, I_pad, Kt;
+  int T, d, H, G, dh, n_tiles, splits, I_pad, Kt, nrb;  // nrb: 32-row blocks in xt
 };
-
-// Contraction order inside a stage of KC columns.  Lane l of a wavefront serves token row
-// (or weight column) l % 32 and the half h = l / 32 of the stage; its k-step s covers stage
-// columns h*KC/2 + 8s .. +7.  Any assignment of contraction indices to (half, k-step)
-// yields the same sums as long as both operands follow it; this one gives every lane one
-// contiguous run of KC bytes of its token row per stage, loaded straight into registers.
-template <int KC>
-struct TokenFrag {
-  u32x4 v[KC / 16];
-};
-
-template <int KC>
-__device__ inline void load_tokens(TokenFrag<KC>& f, const uint16_t* __restrict__ src) {
-#pragma unroll
-  for (int s = 0; s < KC / 16; ++s) f.v[s] = *reinterpret_cast<const u32x4*>(src + 8 * s);
-}
 
 // A stage of a block's weight tile: COLS columns x KC contraction elements spread over
 // NT threads (KC*COLS/(8*NT) 16-byte segments each), staged through registers into LDS rows
@@ -327,12 +343,12 @@ struct WeightStage {
 
 template <int KC, int COLS, int NT>
 __device__ inline void load_weights(WeightStage<KC, COLS, NT>& w, const uint16_t* __restrict__ tile,
-                                    int64_t ld, int k0) {
+                                    int ld, int k0) {
   constexpr int kSegs = WeightStage<KC, COLS, NT>::kSegs;
 #pragma unroll
   for (int j = 0; j < WeightStage<KC, COLS, NT>::kPerThread; ++j) {
-    const int i = threadIdx.x + NT * j;
-    w.v[j] = *reinterpret_cast<const u32x4*>(tile + (int64_t)(i / kSegs) * ld + k0 + 8 * (i % kSegs));
+    const uint32_t i = threadIdx.x + NT * j;
+    w.v[j] = *reinterpret_cast<const u32x4*>(tile + ((i / kSegs) * (uint32_t)ld + k0 + 8 * (i % kSegs)));
   }
 }
 
@@ -346,58 +362,116 @@ __device__ inline void store_weights(const WeightStage<KC, COLS, NT>& w, uint16_
   }
 }
 
-// MFMA work of one stage: the wave's 32 token rows against its 128 weight columns
-// (blocks: gate 0-31, gate 32-63, up 0-31, up 32-63 of its 64 neurons).  ZERO starts the
+// Contraction order inside a stage of KC columns.  Lane l of a wavefront serves token row
+// (or weight column) l % 32 and the half h = l / 32 of the stage; its k-step s covers stage
+// columns h*KC/2 + 8s .. +7.  Any assignment of contraction indices to (half, k-step)
+// yields the same sums as long as both operands follow it; this one gives every lane one
+// contiguous run of KC bytes of each of its token rows per stage, loaded straight into
+// registers.
+template <int KC, int RB>
+struct TokenRows {
+  u32x4 v[RB][KC / 16];
+};
+
+template <int KC, int RB>
+__device__ inline void load_token_rows(TokenRows<KC, RB>& f, const uint16_t* __restrict__ xt,
+                                       const uint32_t (&unit)[RB], int lane) {
+#pragma unroll
+  for (int rb = 0; rb < RB; ++rb)
+#pragma unroll
+    for (int s = 0; s < KC / 16; ++s)
+      f.v[rb][s] = *reinterpret_cast<const u32x4*>(xt + (unit[rb] + 512 * s + 8 * lane));
+}
+
+// MFMA work of one stage: the wave's RB token row blocks against the gate and up
+// fragments of its NB neuron blocks; each LDS fragment feeds RB MFMAs.  ZERO starts the
 // accumulators from zero (first stage of a contraction) instead of adding to them.
-template <int KC, bool ZERO>
-__device__ inline void stage_mfma(const uint16_t* Bs, const TokenFrag<KC>& a, f32x16 (&acc)[4],
-                                  int lane) {
-  const int c = lane & 31;
-  const int off = (lane >> 5) * (KC / 2);
+template <int KC, int RB, int NB, bool ZERO>
+__device__ __forceinline__ void stage_mfma(const uint16_t* B, const TokenRows<KC, RB>& a,
+                                           f32x16 (&acc)[RB][NB][2], const int (&gate_off)[NB],
+                                           const int (&up_off)[NB]) {
 #pragma unroll
   for (int s = 0; s < KC / 16; ++s) {
-    const bf16x8 av = __builtin_bit_cast(bf16x8, a.v[s]);
 #pragma unroll
-    for (int b = 0; b < 4; ++b) {
-      const bf16x8 bv =
-          *reinterpret_cast<const bf16x8*>(Bs + (b * 32 + c) * (KC + 8) + off + 8 * s);
-      acc[b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av, bv, (ZERO && s == 0) ? f32x16{} : acc[b],
-                                                       0, 0, 0);
+    for (int nb = 0; nb < NB; ++nb) {
+      const bf16x8 bg = *reinterpret_cast<const bf16x8*>(B + gate_off[nb] + 8 * s);
+      const bf16x8 bu = *reinterpret_cast<const bf16x8*>(B + up_off[nb] + 8 * s);
+#pragma unroll
+      for (int rb = 0; rb < RB; ++rb) {
+        const bf16x8 av = __builtin_bit_cast(bf16x8, a.v[rb][s]);
+        const bool z = ZERO && s == 0;
+        acc[rb][nb][0] =
+            __builtin_amdgcn_mfma_f32_32x32x16_bf16(av, bg, z ? f32x16{} : acc[rb][nb][0], 0, 0, 0);
+        acc[rb][nb][1] =
+            __builtin_amdgcn_mfma_f32_32x32x16_bf16(av, bu, z ? f32x16{} : acc[rb][nb][1], 0, 0, 0);
+      }
     }
   }
 }
 
-// Block = (WN neuron tiles of 64, token split), WM x WN wavefronts.  For every tile of
-// 32*WM tokens of its split the block runs one contraction over Kt = d + H*dh in stages
-// of KC:
+// Per-lane coefficients c1, c2 of the accumulator elements, either as fp32 or, where
+// registers are short, rounded to bf16 and packed as one 32-bit (c1, c2) pair.
+template <int RB, int NB, bool PACK>
+struct Coefs;
+
+template <int RB, int NB>
+struct Coefs<RB, NB, false> {
+  float v1[RB][NB][16], v2[RB][NB][16];
+  __device__ __forceinline__ void set(int rb, int nb, int i, float a, float b) {
+    v1[rb][nb][i] = a;
+    v2[rb][nb][i] = b;
+  }
+  __device__ __forceinline__ float c1(int rb, int nb, int i) const { return v1[rb][nb][i]; }
+  __device__ __forceinline__ float c2(int rb, int nb, int i) const { return v2[rb][nb][i]; }
+};
+
+template <int RB, int NB>
+struct Coefs<RB, NB, true> {
+  uint32_t v[RB][NB][16];  // c1 in the high half, c2 in the low half
+  __device__ __forceinline__ void set(int rb, int nb, int i, float a, float b) {
+    v[rb][nb][i] = ((uint32_t)f32_to_bf16(a) << 16) | (uint32_t)f32_to_bf16(b);
+  }
+  __device__ __forceinline__ float c1(int rb, int nb, int i) const {
+    return __uint_as_float(v[rb][nb][i] & 0xffff0000u);
+  }
+  __device__ __forceinline__ float c2(int rb, int nb, int i) const {
+    return __uint_as_float(v[rb][nb][i] << 16);
+  }
+};
+
+// Block = (neuron group of 32*NB*WN neurons, token split) with WM x WN wavefronts.  Wave
+// (wm, wn) owns RB 32-row blocks of tokens (rows 32*RB*wm ..) and NB 32-neuron blocks
+// (neurons 32*NB*wn ..), each neuron block held as a gate and an up MFMA accumulator, so
+// c1/c2 and both damage terms of a (token, neuron) pair sit in the same lane.  For every
+// tile of 32*RB*WM tokens of its split the block runs one contraction over
+// Kt = d + H*dh in stages of KC:
 //   stages [0, d/KC)          acc = [x] . [W'_gate | W'_up]^T          -> c1, c2 in registers
 //   each next dh/KC stages    acc = [a_h] . [Fg_h | Fu_h]^T            -> Delta^2 column sums
-// Wave (wm, wn) owns token rows 32wm..32wm+31 and the 128 columns of neuron tile wn, so
-// c1/c2 and both damage terms of a (token, neuron) pair sit in the same lane.  Both
-// operands are fetched two stages ahead into registers: the token rows go straight to
-// the MFMAs, the weight stage shared by the block is written to a double-buffered LDS
-// tile one stage before use.  Rows past the last token are clamped to a real row and
-// given zero coefficients.  Column sums are kept per lane over its 16 rows, folded
-// across the two half-waves after the last query head of each KV group, and banked in
-// LDS per (wave, group); the block writes the fixed-order sum over its WM row waves
-// times ||w^d_k||^2 to its split's partial.
-template <int KC, int WM, int WN>
-__global__ void __launch_bounds__(64 * WM * WN, 8 / (WM * WN))
+// Both operands are fetched two stages ahead into registers: the token fragments (one
+// contiguous 1 KB load per k-step) go straight to the MFMAs, the weight stage shared by
+// the block is written to a double-buffered LDS tile one stage before use, and each LDS
+// fragment feeds RB MFMAs.  Rows past the last token get zero coefficients.  Column sums
+// are kept per lane over its rows, folded across the two half-waves after the last query
+// head of each KV group, and banked in LDS per (wave, group); the block writes the
+// fixed-order sum over its WM row waves times ||w^d_k||^2 to its split's partial.
+template <int KC, int WM, int WN, int RB, int NB, bool PACK>
+__global__ void __launch_bounds__(64 * WM * WN, 2)  // two waves per SIMD
 affinity_bf16_kernel(AffinityArgs p) {
   constexpr int NT = 64 * WM * WN;
-  constexpr int kRows = 32 * WM;
-  constexpr int kStageCols = kCols * WN;
+  constexpr int kRows = 32 * RB * WM;     // tokens per block tile
+  constexpr int kNeurons = 32 * NB * WN;  // neurons per block
+  constexpr int kStageCols = 2 * kNeurons;
+  static_assert(kNeurons % kBN == 0, "a block covers whole 64-neuron tiles");
   using WStage = WeightStage<KC, kStageCols, NT>;
   __shared__ __attribute__((aligned(16))) uint16_t Bs[2][kStageCols * (KC + 8)];
-  extern __shared__ float red[];  // [WM*WN][G][kBN]
+  extern __shared__ float red[];  // [WM*WN][G][32*NB]
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int wm = wave % WM, wn = wave / WM;
-  const int tg = blockIdx.x / p.splits;  // group of WN neuron tiles
+  const int tg = blockIdx.x / p.splits;  // neuron group of this block
   const int split = blockIdx.x % p.splits;
-  const int HD = p.H * p.dh;
   const int hpg = p.H / p.G;
 
-  for (int i = threadIdx.x; i < WM * WN * p.G * kBN; i += NT) red[i] = 0.0f;
+  for (int i = threadIdx.x; i < WM * WN * p.G * 32 * NB; i += NT) red[i] = 0.0f;
 
   const int mtiles = (p.T + kRows - 1) / kRows;
   const int per = (mtiles + p.splits - 1) / p.splits;
@@ -407,27 +481,45 @@ affinity_bf16_kernel(AffinityArgs p) {
   const int nqh = p.dh / KC;  // stages per head
   const int nq = nq1 + p.H * nqh;
   const uint16_t* w_tile = p.wcat + (int64_t)tg * kStageCols * p.Kt;
-  const int bs_off = wn * kCols * (KC + 8);  // this wave's columns inside the LDS stage
+  // LDS offsets of this wave's gate and up fragments inside a weight stage: neuron n of
+  // the block sits at stage row 128*(n/64) + n%64 (gate) and 64 rows further (up).
+  int gate_off[NB], up_off[NB];
+#pragma unroll
+  for (int nb = 0; nb < NB; ++nb) {
+    const int n0 = 32 * (NB * wn + nb);
+    const int row = (n0 / kBN) * kCols + n0 % kBN + (lane & 31);
+    gate_off[nb] = row * (KC + 8) + (lane >> 5) * (KC / 2);
+    up_off[nb] = gate_off[nb] + kBN * (KC + 8);
+  }
   __syncthreads();
 
   for (int mt = mt_begin; mt < mt_end; ++mt) {
     const int m0 = mt * kRows;
-    const int64_t row = min(m0 + wm * 32 + (lane & 31), p.T - 1);
-    const uint16_t* xrow = p.x + row * p.d + (lane >> 5) * (KC / 2);
-    const uint16_t* arow = p.attn + row * HD + (lane >> 5) * (KC / 2) - p.d;
-    auto token_src = [&](int q) { return (q < nq1 ? xrow : arow) + q * KC; };
+    // Row blocks past the last one are clamped to it; their rows get zero coefficients.
+    uint32_t unit0[RB];
+#pragma unroll
+    for (int rb = 0; rb < RB; ++rb)
+      unit0[rb] = (uint32_t)min(mt * RB * WM + RB * wm + rb, p.nrb - 1) * (uint32_t)(32 * p.Kt);
+    auto load_tokens_for = [&](TokenRows<KC, RB>& f, int q) __attribute__((always_inline)) {
+      uint32_t unit[RB];
+#pragma unroll
+      for (int rb = 0; rb < RB; ++rb) unit[rb] = unit0[rb] + q * (32 * KC);
+      load_token_rows<KC, RB>(f, p.xt, unit, lane);
+    };
 
-    f32x16 acc[4];
-    float c1[2][16], c2[2][16];
-    float colsum[2] = {0.0f, 0.0f};
+    f32x16 acc[RB][NB][2];  // [row block][neuron block][gate, up]
+    Coefs<RB, NB, PACK> cf;
+    float colsum[NB];
+#pragma unroll
+    for (int nb = 0; nb < NB; ++nb) colsum[nb] = 0.0f;
     int head_stage = 0;  // stages done of the current head
     int h = 0;
-    TokenFrag<KC> t0, t1, t2;
+    TokenRows<KC, RB> t0, t1, t2;
     WStage w0, w1;
-    load_tokens<KC>(t0, token_src(0));
+    load_tokens_for(t0, 0);
     load_weights(w0, w_tile, p.Kt, 0);
     if (nq > 1) {
-      load_tokens<KC>(t1, token_src(1));
+      load_tokens_for(t1, 1);
       load_weights(w1, w_tile, p.Kt, KC);
     }
     store_weights(w0, Bs[0]);
@@ -435,48 +527,53 @@ affinity_bf16_kernel(AffinityArgs p) {
 
     // Stage q: tokens in `cur`, stage q+1's weights in `wnext` (stored to LDS here),
     // stage q+2 fetched into `tnew` / `wnew`.
-    auto stage = [&](int q, TokenFrag<KC>& cur, TokenFrag<KC>& tnew, WStage& wnext,
-                     WStage& wnew) {
+    auto stage = [&](int q, TokenRows<KC, RB>& cur, TokenRows<KC, RB>& tnew, WStage& wnext,
+                     WStage& wnew) __attribute__((always_inline)) {
       const int buf = q & 1;
       if (q + 2 < nq) {
-        load_tokens<KC>(tnew, token_src(q + 2));
+        load_tokens_for(tnew, q + 2);
         load_weights(wnew, w_tile, p.Kt, (q + 2) * KC);
       }
       if (q == 0 || (q >= nq1 && head_stage == 0))
-        stage_mfma<KC, true>(Bs[buf] + bs_off, cur, acc, lane);
+        stage_mfma<KC, RB, NB, true>(Bs[buf], cur, acc, gate_off, up_off);
       else
-        stage_mfma<KC, false>(Bs[buf] + bs_off, cur, acc, lane);
+        stage_mfma<KC, RB, NB, false>(Bs[buf], cur, acc, gate_off, up_off);
       if (q == nq1 - 1) {
         // Operating point: g, u -> c1 = silu'(g) u / r, c2 = silu(g) / r.
 #pragma unroll
-        for (int i = 0; i < 16; ++i) {
-          const int r = m0 + wm * 32 + acc_row(i, lane);
-          const float ri = r < p.T ? p.rinv[r] : 0.0f;
+        for (int rb = 0; rb < RB; ++rb)
 #pragma unroll
-          for (int j = 0; j < 2; ++j) {
-            const float g = acc[j][i] * ri;
-            const float u = acc[2 + j][i] * ri;
-            const float sg = __builtin_amdgcn_rcpf(1.0f + __expf(-g));
-            c2[j][i] = g * sg * ri;
-            c1[j][i] = sg * (1.0f + g * (1.0f - sg)) * u * ri;
+          for (int i = 0; i < 16; ++i) {
+            const int r = m0 + 32 * (RB * wm + rb) + acc_row(i, lane);
+            const float ri = r < p.T ? p.rinv[r] : 0.0f;
+#pragma unroll
+            for (int nb = 0; nb < NB; ++nb) {
+              const float g = acc[rb][nb][0][i] * ri;
+              const float u = acc[rb][nb][1][i] * ri;
+              const float sg = __builtin_amdgcn_rcpf(1.0f + __expf(-g));
+              cf.set(rb, nb, i, sg * (1.0f + g * (1.0f - sg)) * u * ri, g * sg * ri);
+            }
           }
-        }
       } else if (q >= nq1 && ++head_stage == nqh) {
         // Head h done: Delta = c1 (a_h . Fg) + c2 (a_h . Fu); sum Delta^2 over the rows.
 #pragma unroll
-        for (int j = 0; j < 2; ++j)
+        for (int rb = 0; rb < RB; ++rb)
 #pragma unroll
-          for (int i = 0; i < 16; ++i) {
-            const float dl = c1[j][i] * acc[j][i] + c2[j][i] * acc[2 + j][i];
-            colsum[j] = fmaf(dl, dl, colsum[j]);
-          }
+          for (int nb = 0; nb < NB; ++nb)
+#pragma unroll
+            for (int i = 0; i < 16; ++i) {
+              const float dl = cf.c1(rb, nb, i) * acc[rb][nb][0][i] + cf.c2(rb, nb, i) * acc[rb][nb][1][i];
+              colsum[nb] = fmaf(dl, dl, colsum[nb]);
+            }
         head_stage = 0;
         if (h % hpg == hpg - 1) {
           // Last query head of its KV group: fold the two half-waves and bank the sums.
-          const float s0 = colsum[0] + __shfl_xor(colsum[0], 32, 64);
-          const float s1 = colsum[1] + __shfl_xor(colsum[1], 32, 64);
-          red[(wave * p.G + h / hpg) * kBN + lane] += (lane < 32) ? s0 : s1;
-          colsum[0] = colsum[1] = 0.0f;
+#pragma unroll
+          for (int nb = 0; nb < NB; ++nb) {
+            const float t = colsum[nb] + __shfl_xor(colsum[nb], 32, 64);
+            if (lane < 32) red[(wave * p.G + h / hpg) * (32 * NB) + 32 * nb + lane] += t;
+            colsum[nb] = 0.0f;
+          }
         }
         ++h;
       }
@@ -502,25 +599,27 @@ affinity_bf16_kernel(AffinityArgs p) {
   }
 
   // Sum the row waves in a fixed order and scale by ||w^d_k||^2.
-  for (int i = threadIdx.x; i < p.G * kBN * WN; i += NT) {
-    const int g = i / (kBN * WN), nl = i % (kBN * WN);
-    const int cw = nl / kBN, k = nl % kBN;
-    float s = 0.0f;
-    for (int w = 0; w < WM; ++w) s += red[((cw * WM + w) * p.G + g) * kBN + k];
-    const int n = tg * kBN * WN + nl;
-    p.partial[((int64_t)split * p.G + g) * p.I_pad + n] = s * p.nd[n];
+  for (int i = threadIdx.x; i < p.G * kNeurons; i += NT) {
+    const int g = i / kNeurons, nl = i % kNeurons;
+    const int cw = nl / (32 * NB), k = nl % (32 * NB);
+    float sum = 0.0f;
+    for (int w = 0; w < WM; ++w) sum += red[((cw * WM + w) * p.G + g) * (32 * NB) + k];
+    const int n = tg * kNeurons + nl;
+    p.partial[((int64_t)split * p.G + g) * p.I_pad + n] = sum * p.nd[n];
   }
 }
 
-// Launch shape of the bf16 affinity kernel for one slice of T tokens.
-struct AffinityLaunch {
-  int kc, wm, wn;
-};
-
-template <int KC, int WM, int WN>
-void launch_affinity(const AffinityArgs& p, int n_tiles, hipStream_t s) {
-  const size_t shm = sizeof(float) * WM * WN * p.G * kBN;
-  affinity_bf16_kernel<KC, WM, WN><<<(n_tiles / WN) * p.splits, 64 * WM * WN, shm, s>>>(p);
+// Launches the fused kernel on one slice; returns the number of token splits used.
+template <int KC, int WM, int WN, int RB, int NB, bool PACK = false>
+int launch_affinity(AffinityArgs p, hipStream_t s) {
+  constexpr int kRows = 32 * RB * WM;
+  constexpr int kNeurons = 32 * NB * WN;
+  const int groups = p.n_tiles * kBN / kNeurons;
+  const int mtiles = (p.T + kRows - 1) / kRows;
+  p.splits = std::max(1, std::min((kTargetBlocks + groups - 1) / groups, std::min(mtiles, kMaxSplits)));
+  const size_t shm = sizeof(float) * WM * WN * p.G * 32 * NB;
+  affinity_bf16_kernel<KC, WM, WN, RB, NB, PACK><<<groups * p.splits, 64 * WM * WN, shm, s>>>(p);
+  return p.splits;
 }
 
 // ------------------------------------------------------------------ fused affinity (fp32)
@@ -622,6 +721,8 @@ struct dtp_layer_s {
   float* nd = nullptr;       // [I_pad]
   float* rinv = nullptr;     // [kSliceTokens]
   float* partial = nullptr;  // [kMaxSplits][G][I_pad]
+  uint16_t* xt = nullptr;    // bf16 path: one slice of tiled token rows
+  int64_t tile_slice = 0;    // tokens per bf16 slice
   bool profiling = false;
   std::vector<std::pair<hipEvent_t, hipEvent_t>> events;
 };
@@ -629,7 +730,7 @@ struct dtp_layer_s {
 namespace {
 
 void layer_free(dtp_layer L) {
-  void* bufs[] = {L->w, L->woT, L->fold32, L->nd, L->rinv, L->partial};
+  void* bufs[] = {L->w, L->woT, L->fold32, L->nd, L->rinv, L->partial, L->xt};
   for (void* b : bufs)
     if (b) (void)hipFree(b);
   for (auto& e : L->events) {
@@ -684,8 +785,11 @@ dtp_status dtp_layer_create(const dtp_layer_desc* desc, dtp_layer* out) {
   const size_t rows = (size_t)L->n_tiles * kCols;
   if (d.dtype == DTP_BF16) {
     L->Kt = d.d_model + (int)HD;
+    // Element offsets inside the tiled slice stay below 2^30.
+    L->tile_slice = std::max<int64_t>(256, std::min<int64_t>(kTileTokens, ((int64_t)1 << 30) / L->Kt) / 256 * 256);
     if (e == hipSuccess) e = hipMalloc(&L->w, 2 * rows * L->Kt);
     if (e == hipSuccess) e = hipMalloc(&L->woT, 2 * (size_t)HD * d.d_model);
+    if (e == hipSuccess) e = hipMalloc(&L->xt, 2 * (size_t)L->tile_slice * L->Kt);
   } else {
     L->Kt = d.d_model;
     if (e == hipSuccess) e = hipMalloc(&L->w, 4 * rows * d.d_model);
@@ -772,8 +876,12 @@ dtp_status dtp_affinity_accumulate(dtp_layer L, const void* x, const void* attn,
   const int H = d.n_q_heads, dh = d.head_dim, HD = H * dh, G = d.n_kv_groups;
   const int I = d.n_neurons, dm = d.d_model;
   const size_t esz = d.dtype == DTP_BF16 ? 2 : 4;
-  for (int64_t t0 = 0; t0 < n_tokens; t0 += kSliceTokens) {
-    const int T = (int)std::min<int64_t>(kSliceTokens, n_tokens - t0);
+  // Tokens per slice: the 1/r buffer size, and element offsets of a slice below 2^30.
+  const int64_t width = std::max(dm, HD);
+  int64_t slice = std::max<int64_t>(256, std::min<int64_t>(kSliceTokens, ((int64_t)1 << 30) / width) / 256 * 256);
+  if (d.dtype == DTP_BF16) slice = std::min(slice, L->tile_slice);
+  for (int64_t t0 = 0; t0 < n_tokens; t0 += slice) {
+    const int T = (int)std::min<int64_t>(slice, n_tokens - t0);
     const char* xs = (const char*)x + esz * (size_t)t0 * dm;
     const char* as = (const char*)attn + esz * (size_t)t0 * HD;
     const unsigned rb = (unsigned)((T + 3) / 4);
@@ -782,6 +890,24 @@ dtp_status dtp_affinity_accumulate(dtp_layer L, const void* x, const void* attn,
     else
       rms_kernel<float><<<rb, 256, 0, s>>>((const float*)xs, T, dm, d.rms_eps, L->rinv);
     DTP_HIP(hipGetLastError());
+    // bf16: rewrite the slice's token rows into the fragment-contiguous layout.  Stages
+    // are as deep as the operating point and the heads both divide.
+    const int kc = dm % 64 == 0 && dh % 64 == 0 ? 64 : dm % 32 == 0 && dh % 32 == 0 ? 32 : 16;
+    const int nrb = (T + 31) / 32;
+    if (d.dtype == DTP_BF16) {
+      const int64_t n_chunks = (int64_t)nrb * 32 * L->Kt / 8;
+      const unsigned tgrid = (unsigned)((n_chunks + 255) / 256);
+      if (kc == 64)
+        tile_tokens_kernel<64><<<tgrid, 256, 0, s>>>((const uint16_t*)xs, (const uint16_t*)as, T, dm,
+                                                     HD, L->Kt / kc, n_chunks, L->xt);
+      else if (kc == 32)
+        tile_tokens_kernel<32><<<tgrid, 256, 0, s>>>((const uint16_t*)xs, (const uint16_t*)as, T, dm,
+                                                     HD, L->Kt / kc, n_chunks, L->xt);
+      else
+        tile_tokens_kernel<16><<<tgrid, 256, 0, s>>>((const uint16_t*)xs, (const uint16_t*)as, T, dm,
+                                                     HD, L->Kt / kc, n_chunks, L->xt);
+      DTP_HIP(hipGetLastError());
+    }
 
     int splits;
     hipEvent_t e0 = nullptr, e1 = nullptr;
@@ -792,8 +918,7 @@ dtp_status dtp_affinity_accumulate(dtp_layer L, const void* x, const void* attn,
     }
     if (d.dtype == DTP_BF16) {
       AffinityArgs p;
-      p.x = (const uint16_t*)xs;
-      p.attn = (const uint16_t*)as;
+      p.xt = L->xt;
       p.wcat = (const uint16_t*)L->w;
       p.rinv = L->rinv;
       p.nd = L->nd;
@@ -806,16 +931,16 @@ dtp_status dtp_affinity_accumulate(dtp_layer L, const void* x, const void* attn,
       p.n_tiles = L->n_tiles;
       p.I_pad = L->I_pad;
       p.Kt = L->Kt;
-      const bool kc32 = dm % 32 == 0 && dh % 32 == 0;
-      const int rows = 128;  // 32 * WM
-      const int mtiles = (T + rows - 1) / rows;
-      splits = (kTargetBlocks + L->n_tiles - 1) / L->n_tiles;
-      splits = std::max(1, std::min(splits, std::min(mtiles, kMaxSplits)));
-      p.splits = splits;
-      if (kc32)
-        launch_affinity<32, 4, 1>(p, L->n_tiles, s);
+      p.nrb = nrb;
+      p.splits = 0;
+      // Eight wavefronts per block (one block per CU): 256 tokens x 64 neurons per tile;
+      // four for 16-wide stages, whose weight stage has only 256 16-byte pieces.
+      if (kc == 64)
+        splits = launch_affinity<64, 8, 1, 1, 2>(p, s);
+      else if (kc == 32)
+        splits = launch_affinity<32, 8, 1, 1, 2>(p, s);
       else
-        launch_affinity<16, 4, 1>(p, L->n_tiles, s);
+        splits = launch_affinity<16, 4, 1, 1, 2>(p, s);
     } else {
       splits = (kTargetBlocks / 4 + L->n_tiles - 1) / L->n_tiles;
       splits = std::max(1, std::min(splits, std::min(T, kMaxSplits)));
