@@ -295,12 +295,32 @@ rms_kernel(const T* __restrict__ x, int64_t T_tokens, int d, float eps, float* _
 // tokens is therefore first rewritten so that every fragment is one contiguous 1 KB run:
 //   xt[rb][q][s][h][r][e] = [x | attn][32*rb + r][q*KC + h*KC/2 + 8*s + e]
 // for 32-row block rb, stage q of KC columns, k-step s < KC/16, half h, row r < 32 and
-// element e < 8 (rows past the last token are zero).  One thread moves one 16-byte chunk;
-// consecutive threads read consecutive chunks of a row.
+// element e < 8 (rows past the last token are zero).  The head entries of token t are
+// multiplied by p_t = pow2_floor(1/r_t), which is exact in bf16, so the per-head
+// contractions come out as p_t (a_h . F) and the damage coefficients c1/p_t, c2/p_t that
+// multiply them lie within a factor 2 of silu'(g) u and silu(g) (fp16 range, whatever
+// the token scale).  One thread moves one 16-byte chunk; consecutive threads read
+// consecutive chunks of a row.
+__device__ __forceinline__ float pow2_floor(float v) {  // 2^floor(log2 v), v normal and > 0
+  return __uint_as_float(__float_as_uint(v) & 0x7f800000u);
+}
+
+__device__ __forceinline__ float pow2_fraction(float v) {  // v / pow2_floor(v), in [1, 2)
+  return __uint_as_float((__float_as_uint(v) & 0x007fffffu) | 0x3f800000u);
+}
+
+__device__ __forceinline__ uint32_t scale_bf16_pair(uint32_t w, float f) {
+  // Both halves times a power of two; exact while the results stay normal.
+  const float lo = __uint_as_float(w << 16) * f;
+  const float hi = __uint_as_float(w & 0xffff0000u) * f;
+  return (__float_as_uint(lo) >> 16) | (__float_as_uint(hi) & 0xffff0000u);
+}
+
 template <int KC>
 __global__ void __launch_bounds__(256)
-tile_tokens_kernel(const uint16_t* __restrict__ x, const uint16_t* __restrict__ attn, int T, int d,
-                   int HD, int nq, int64_t n_chunks, uint16_t* __restrict__ xt) {
+tile_tokens_kernel(const uint16_t* __restrict__ x, const uint16_t* __restrict__ attn,
+                   const float* __restrict__ rinv, int T, int d, int HD, int nq, int64_t n_chunks,
+                   uint16_t* __restrict__ xt) {
   constexpr int kRowChunks = KC / 8;
   constexpr int kUnitChunks = 32 * kRowChunks;
   const int64_t g = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
@@ -313,9 +333,16 @@ tile_tokens_kernel(const uint16_t* __restrict__ x, const uint16_t* __restrict__ 
   const int64_t t = 32 * rb + r;
   const int k0 = q * KC + 8 * c;
   u32x4 v = {0u, 0u, 0u, 0u};
-  if (t < T)
-    v = k0 < d ? *reinterpret_cast<const u32x4*>(x + t * d + k0)
-               : *reinterpret_cast<const u32x4*>(attn + t * HD + (k0 - d));
+  if (t < T) {
+    if (k0 < d) {
+      v = *reinterpret_cast<const u32x4*>(x + t * d + k0);
+    } else {
+      v = *reinterpret_cast<const u32x4*>(attn + t * HD + (k0 - d));
+      const float f = pow2_floor(rinv[t]);
+#pragma unroll
+      for (int j = 0; j < 4; ++j) v[j] = scale_bf16_pair(v[j], f);
+    }
+  }
   const int h = c / (KC / 16), s = c % (KC / 16);
   *reinterpret_cast<u32x4*>(xt + u * (32 * KC) + ((s * 2 + h) * 32 + r) * 8) = v;
 }
@@ -384,33 +411,54 @@ __device__ inline void load_token_rows(TokenRows<KC, RB>& f, const uint16_t* __r
 }
 
 // MFMA work of one stage: the wave's RB token row blocks against the gate and up
-// fragments of its NB neuron blocks; each LDS fragment feeds RB MFMAs.  ZERO starts the
-// accumulators from zero (first stage of a contraction) instead of adding to them.
+// fragments of its NB neuron blocks; each LDS fragment feeds RB MFMAs.  Fragments are
+// read two k-steps ahead of their MFMAs (double-buffered in registers), so an MFMA never
+// waits on the LDS read it consumes.  ZERO starts the accumulators from zero (first stage of a
+// contraction) instead of adding to them.
 template <int KC, int RB, int NB, bool ZERO>
 __device__ __forceinline__ void stage_mfma(const uint16_t* B, const TokenRows<KC, RB>& a,
                                            f32x16 (&acc)[RB][NB][2], const int (&gate_off)[NB],
                                            const int (&up_off)[NB]) {
-#pragma unroll
-  for (int s = 0; s < KC / 16; ++s) {
+  constexpr int kSteps = KC / 16;
+  bf16x8 frag[2][NB][2];
+  auto read = [&](int buf, int s) __attribute__((always_inline)) {
 #pragma unroll
     for (int nb = 0; nb < NB; ++nb) {
-      const bf16x8 bg = *reinterpret_cast<const bf16x8*>(B + gate_off[nb] + 8 * s);
-      const bf16x8 bu = *reinterpret_cast<const bf16x8*>(B + up_off[nb] + 8 * s);
+      frag[buf][nb][0] = *reinterpret_cast<const bf16x8*>(B + gate_off[nb] + 8 * s);
+      frag[buf][nb][1] = *reinterpret_cast<const bf16x8*>(B + up_off[nb] + 8 * s);
+    }
+  };
+  read(0, 0);
+  if (kSteps > 1) read(1, 1);
+#pragma unroll
+  for (int s = 0; s < kSteps; ++s) {
+#pragma unroll
+    for (int nb = 0; nb < NB; ++nb)
 #pragma unroll
       for (int rb = 0; rb < RB; ++rb) {
         const bf16x8 av = __builtin_bit_cast(bf16x8, a.v[rb][s]);
         const bool z = ZERO && s == 0;
-        acc[rb][nb][0] =
-            __builtin_amdgcn_mfma_f32_32x32x16_bf16(av, bg, z ? f32x16{} : acc[rb][nb][0], 0, 0, 0);
-        acc[rb][nb][1] =
-            __builtin_amdgcn_mfma_f32_32x32x16_bf16(av, bu, z ? f32x16{} : acc[rb][nb][1], 0, 0, 0);
+#pragma unroll
+        for (int gu = 0; gu < 2; ++gu)
+          acc[rb][nb][gu] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+              av, frag[s & 1][nb][gu], z ? f32x16{} : acc[rb][nb][gu], 0, 0, 0);
       }
-    }
+    if (s + 2 < kSteps) read(s & 1, s + 2);
+  }
+  // Keep that order through scheduling: the reads of k-steps 0 and 1 first, then each
+  // k-step's MFMAs followed by the reads of the k-step after next.
+  constexpr int kFrags = 2 * NB, kMfma = 2 * NB * RB;
+  __builtin_amdgcn_sched_group_barrier(0x100, kSteps > 1 ? 2 * kFrags : kFrags, 0);
+#pragma unroll
+  for (int s = 0; s < kSteps; ++s) {
+    __builtin_amdgcn_sched_group_barrier(0x008, kMfma, 0);
+    if (s + 2 < kSteps) __builtin_amdgcn_sched_group_barrier(0x100, kFrags, 0);
   }
 }
 
-// Per-lane coefficients c1, c2 of the accumulator elements, either as fp32 or, where
-// registers are short, rounded to bf16 and packed as one 32-bit (c1, c2) pair.
+// Per-lane coefficients c1/p_t and c2/p_t of the accumulator elements, either as fp32 or
+// rounded to fp16 and packed as one 32-bit (c1, c2) pair (fp16 keeps 11 significant
+// bits, and the scaled coefficients lie within a factor 2 of silu'(g) u and silu(g)).
 template <int RB, int NB, bool PACK>
 struct Coefs;
 
@@ -427,15 +475,16 @@ struct Coefs<RB, NB, false> {
 
 template <int RB, int NB>
 struct Coefs<RB, NB, true> {
-  uint32_t v[RB][NB][16];  // c1 in the high half, c2 in the low half
+  uint32_t v[RB][NB][16];  // c1 in the low half, c2 in the high half
   __device__ __forceinline__ void set(int rb, int nb, int i, float a, float b) {
-    v[rb][nb][i] = ((uint32_t)f32_to_bf16(a) << 16) | (uint32_t)f32_to_bf16(b);
+    v[rb][nb][i] = (uint32_t)__builtin_bit_cast(uint16_t, (_Float16)a) |
+                   ((uint32_t)__builtin_bit_cast(uint16_t, (_Float16)b) << 16);
   }
   __device__ __forceinline__ float c1(int rb, int nb, int i) const {
-    return __uint_as_float(v[rb][nb][i] & 0xffff0000u);
+    return (float)__builtin_bit_cast(_Float16, (uint16_t)(v[rb][nb][i] & 0xffffu));
   }
   __device__ __forceinline__ float c2(int rb, int nb, int i) const {
-    return __uint_as_float(v[rb][nb][i] << 16);
+    return (float)__builtin_bit_cast(_Float16, (uint16_t)(v[rb][nb][i] >> 16));
   }
 };
 
@@ -464,6 +513,7 @@ affinity_bf16_kernel(AffinityArgs p) {
   static_assert(kNeurons % kBN == 0, "a block covers whole 64-neuron tiles");
   using WStage = WeightStage<KC, kStageCols, NT>;
   __shared__ __attribute__((aligned(16))) uint16_t Bs[2][kStageCols * (KC + 8)];
+  __shared__ __attribute__((aligned(16))) float rv[kRows];  // 1/r of the tile's rows, 0 past T
   extern __shared__ float red[];  // [WM*WN][G][32*NB]
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int wm = wave % WM, wn = wave / WM;
@@ -518,11 +568,10 @@ affinity_bf16_kernel(AffinityArgs p) {
     WStage w0, w1;
     load_tokens_for(t0, 0);
     load_weights(w0, w_tile, p.Kt, 0);
-    if (nq > 1) {
-      load_tokens_for(t1, 1);
-      load_weights(w1, w_tile, p.Kt, KC);
-    }
+    load_tokens_for(t1, min(1, nq - 1));
+    load_weights(w1, w_tile, p.Kt, min(1, nq - 1) * KC);
     store_weights(w0, Bs[0]);
+    for (int i = threadIdx.x; i < kRows; i += NT) rv[i] = m0 + i < p.T ? p.rinv[m0 + i] : 0.0f;
     __syncthreads();
 
     // Stage q: tokens in `cur`, stage q+1's weights in `wnext` (stored to LDS here),
@@ -530,28 +579,36 @@ affinity_bf16_kernel(AffinityArgs p) {
     auto stage = [&](int q, TokenRows<KC, RB>& cur, TokenRows<KC, RB>& tnew, WStage& wnext,
                      WStage& wnew) __attribute__((always_inline)) {
       const int buf = q & 1;
-      if (q + 2 < nq) {
-        load_tokens_for(tnew, q + 2);
-        load_weights(wnew, w_tile, p.Kt, (q + 2) * KC);
-      }
+      // Unconditional (the last two stages re-fetch the last stage), so that the wait
+      // counts before each use stay exact instead of falling back to a full drain.
+      const int qn = min(q + 2, nq - 1);
+      load_tokens_for(tnew, qn);
+      load_weights(wnew, w_tile, p.Kt, qn * KC);
       if (q == 0 || (q >= nq1 && head_stage == 0))
         stage_mfma<KC, RB, NB, true>(Bs[buf], cur, acc, gate_off, up_off);
       else
         stage_mfma<KC, RB, NB, false>(Bs[buf], cur, acc, gate_off, up_off);
       if (q == nq1 - 1) {
-        // Operating point: g, u -> c1 = silu'(g) u / r, c2 = silu(g) / r.
+        // Operating point: g, u -> c1 = silu'(g) u / r, c2 = silu(g) / r, stored divided
+        // by p_t (the head entries were multiplied by it).  Lane l's element i is row
+        // 8(i/4) + 4(l/32) + i%4 of its row block: four runs of four rows.
 #pragma unroll
         for (int rb = 0; rb < RB; ++rb)
 #pragma unroll
-          for (int i = 0; i < 16; ++i) {
-            const int r = m0 + 32 * (RB * wm + rb) + acc_row(i, lane);
-            const float ri = r < p.T ? p.rinv[r] : 0.0f;
+          for (int j = 0; j < 4; ++j) {
+            const float4 r4 = *reinterpret_cast<const float4*>(rv + 32 * (RB * wm + rb) + 8 * j + 4 * (lane >> 5));
 #pragma unroll
-            for (int nb = 0; nb < NB; ++nb) {
-              const float g = acc[rb][nb][0][i] * ri;
-              const float u = acc[rb][nb][1][i] * ri;
-              const float sg = __builtin_amdgcn_rcpf(1.0f + __expf(-g));
-              cf.set(rb, nb, i, sg * (1.0f + g * (1.0f - sg)) * u * ri, g * sg * ri);
+            for (int k = 0; k < 4; ++k) {
+              const int i = 4 * j + k;
+              const float ri = r4[k];
+              const float rs = ri > 0.0f ? pow2_fraction(ri) : 0.0f;  // ri / p_t
+#pragma unroll
+              for (int nb = 0; nb < NB; ++nb) {
+                const float g = acc[rb][nb][0][i] * ri;
+                const float u = acc[rb][nb][1][i] * ri;
+                const float sg = __builtin_amdgcn_rcpf(1.0f + __expf(-g));
+                cf.set(rb, nb, i, sg * (1.0f + g * (1.0f - sg)) * u * rs, g * sg * rs);
+              }
             }
           }
       } else if (q >= nq1 && ++head_stage == nqh) {
@@ -577,7 +634,7 @@ affinity_bf16_kernel(AffinityArgs p) {
         }
         ++h;
       }
-      if (q + 1 < nq) store_weights(wnext, Bs[buf ^ 1]);
+      store_weights(wnext, Bs[buf ^ 1]);  // unused after the last stage
       __syncthreads();
     };
 
@@ -898,14 +955,14 @@ dtp_status dtp_affinity_accumulate(dtp_layer L, const void* x, const void* attn,
       const int64_t n_chunks = (int64_t)nrb * 32 * L->Kt / 8;
       const unsigned tgrid = (unsigned)((n_chunks + 255) / 256);
       if (kc == 64)
-        tile_tokens_kernel<64><<<tgrid, 256, 0, s>>>((const uint16_t*)xs, (const uint16_t*)as, T, dm,
-                                                     HD, L->Kt / kc, n_chunks, L->xt);
+        tile_tokens_kernel<64><<<tgrid, 256, 0, s>>>((const uint16_t*)xs, (const uint16_t*)as, L->rinv, T,
+                                                     dm, HD, L->Kt / kc, n_chunks, L->xt);
       else if (kc == 32)
-        tile_tokens_kernel<32><<<tgrid, 256, 0, s>>>((const uint16_t*)xs, (const uint16_t*)as, T, dm,
-                                                     HD, L->Kt / kc, n_chunks, L->xt);
+        tile_tokens_kernel<32><<<tgrid, 256, 0, s>>>((const uint16_t*)xs, (const uint16_t*)as, L->rinv, T,
+                                                     dm, HD, L->Kt / kc, n_chunks, L->xt);
       else
-        tile_tokens_kernel<16><<<tgrid, 256, 0, s>>>((const uint16_t*)xs, (const uint16_t*)as, T, dm,
-                                                     HD, L->Kt / kc, n_chunks, L->xt);
+        tile_tokens_kernel<16><<<tgrid, 256, 0, s>>>((const uint16_t*)xs, (const uint16_t*)as, L->rinv, T,
+                                                     dm, HD, L->Kt / kc, n_chunks, L->xt);
       DTP_HIP(hipGetLastError());
     }
 
@@ -936,11 +993,11 @@ dtp_status dtp_affinity_accumulate(dtp_layer L, const void* x, const void* attn,
       // Eight wavefronts per block (one block per CU): 256 tokens x 64 neurons per tile;
       // four for 16-wide stages, whose weight stage has only 256 16-byte pieces.
       if (kc == 64)
-        splits = launch_affinity<64, 8, 1, 1, 2>(p, s);
+        splits = launch_affinity<64, 8, 1, 1, 2, true>(p, s);
       else if (kc == 32)
-        splits = launch_affinity<32, 8, 1, 1, 2>(p, s);
+        splits = launch_affinity<32, 8, 1, 1, 2, true>(p, s);
       else
-        splits = launch_affinity<16, 4, 1, 1, 2>(p, s);
+        splits = launch_affinity<16, 4, 1, 1, 2, true>(p, s);
     } else {
       splits = (kTargetBlocks / 4 + L->n_tiles - 1) / L->n_tiles;
       splits = std::max(1, std::min(splits, std::min(T, kMaxSplits)));
