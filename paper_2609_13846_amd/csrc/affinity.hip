@@ -488,6 +488,27 @@ struct Coefs<RB, NB, true> {
   }
 };
 
+// Work item of block b.  Blocks are dealt to the 8 XCDs round-robin (block b runs on
+// XCD b % 8), and each XCD has its own L2.  The (neuron group, token split) items are
+// ordered in bands of SG splits, neuron group by neuron group inside a band, and each
+// XCD takes one contiguous run of that order, so the blocks an XCD runs together share
+// SG token tiles and a few weight tiles.  SG = 0 keeps the plain order.
+template <int SG>
+__device__ __forceinline__ void block_work(int b, int n_tg, int n_split, int& tg, int& split) {
+  if (SG == 0) {
+    tg = b / n_split;
+    split = b % n_split;
+    return;
+  }
+  const int n = n_tg * n_split;
+  const int x = b % 8, slot = b / 8;
+  const int j = x * (n / 8) + min(x, n % 8) + slot;
+  const int g = j / (SG * n_tg), r = j % (SG * n_tg);
+  const int gw = min(SG, n_split - SG * g);
+  tg = r / gw;
+  split = SG * g + r % gw;
+}
+
 // Block = (neuron group of 32*NB*WN neurons, token split) with WM x WN wavefronts.  Wave
 // (wm, wn) owns RB 32-row blocks of tokens (rows 32*RB*wm ..) and NB 32-neuron blocks
 // (neurons 32*NB*wn ..), each neuron block held as a gate and an up MFMA accumulator, so
@@ -503,7 +524,7 @@ struct Coefs<RB, NB, true> {
 // are kept per lane over its rows, folded across the two half-waves after the last query
 // head of each KV group, and banked in LDS per (wave, group); the block writes the
 // fixed-order sum over its WM row waves times ||w^d_k||^2 to its split's partial.
-template <int KC, int WM, int WN, int RB, int NB, bool PACK>
+template <int KC, int WM, int WN, int RB, int NB, bool PACK, int SG>
 __global__ void __launch_bounds__(64 * WM * WN, 2)  // two waves per SIMD
 affinity_bf16_kernel(AffinityArgs p) {
   constexpr int NT = 64 * WM * WN;
@@ -517,8 +538,8 @@ affinity_bf16_kernel(AffinityArgs p) {
   extern __shared__ float red[];  // [WM*WN][G][32*NB]
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int wm = wave % WM, wn = wave / WM;
-  const int tg = blockIdx.x / p.splits;  // neuron group of this block
-  const int split = blockIdx.x % p.splits;
+  int tg, split;  // neuron group and token split of this block
+  block_work<SG>(blockIdx.x, (int)gridDim.x / p.splits, p.splits, tg, split);
   const int hpg = p.H / p.G;
 
   for (int i = threadIdx.x; i < WM * WN * p.G * 32 * NB; i += NT) red[i] = 0.0f;
@@ -667,7 +688,7 @@ affinity_bf16_kernel(AffinityArgs p) {
 }
 
 // Launches the fused kernel on one slice; returns the number of token splits used.
-template <int KC, int WM, int WN, int RB, int NB, bool PACK = false>
+template <int KC, int WM, int WN, int RB, int NB, bool PACK = false, int SG = 4>
 int launch_affinity(AffinityArgs p, hipStream_t s) {
   constexpr int kRows = 32 * RB * WM;
   constexpr int kNeurons = 32 * NB * WN;
@@ -675,7 +696,7 @@ int launch_affinity(AffinityArgs p, hipStream_t s) {
   const int mtiles = (p.T + kRows - 1) / kRows;
   p.splits = std::max(1, std::min((kTargetBlocks + groups - 1) / groups, std::min(mtiles, kMaxSplits)));
   const size_t shm = sizeof(float) * WM * WN * p.G * 32 * NB;
-  affinity_bf16_kernel<KC, WM, WN, RB, NB, PACK><<<groups * p.splits, 64 * WM * WN, shm, s>>>(p);
+  affinity_bf16_kernel<KC, WM, WN, RB, NB, PACK, SG><<<groups * p.splits, 64 * WM * WN, shm, s>>>(p);
   return p.splits;
 }
 

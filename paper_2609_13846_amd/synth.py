@@ -141,6 +141,28 @@ def host_weights(wl: Workload, layer: int) -> LayerWeights:
                         store(w_up, wl.dtype), store(w_down, wl.dtype), outl.astype(np.int64))
 
 
+@dataclasses.dataclass
+class AttnWeights:
+    """Attention-side weights of a layer, used by the down edge into that layer."""
+    w_q: np.ndarray      # [H*dh, d]  (q_proj.weight layout)
+    w_k: np.ndarray      # [G*dh, d]
+    w_v: np.ndarray      # [G*dh, d]
+    gamma: np.ndarray    # [d]        attention pre-norm gain
+
+
+def host_attn_weights(wl: Workload, layer: int) -> AttnWeights:
+    """Seeded q/k/v projections and attention pre-norm gain of a layer (own stream)."""
+    d, HD, GD = wl.d_model, wl.attn_width, wl.n_kv_groups * wl.head_dim
+    g = _rng(wl, layer, 0, 1)
+    s = wl.weight_std
+    w_q = g.standard_normal((HD, d)) * s
+    w_k = g.standard_normal((GD, d)) * s
+    w_v = g.standard_normal((GD, d)) * s
+    gamma = 1.0 + g.standard_normal(d) * wl.gamma_std
+    return AttnWeights(store(w_q, wl.dtype), store(w_k, wl.dtype), store(w_v, wl.dtype),
+                       store(gamma, wl.dtype))
+
+
 def _heads(g: np.random.Generator, wl: Workload, n: int) -> np.ndarray:
     shape = (n, wl.n_q_heads, wl.head_dim)
     if wl.heads_dist == "normal":
@@ -151,11 +173,14 @@ def _heads(g: np.random.Generator, wl: Workload, n: int) -> np.ndarray:
 
 
 def host_tokens(wl: Workload, layer: int, weights: LayerWeights, n_tokens: int,
-                chunk: int = 0) -> tuple:
+                chunk: int = 0, with_pre: bool = False) -> tuple:
     """(x [T,d], attn [T,H,dh]) in storage dtype for chunk ``chunk`` of a layer.
 
-    Rows are drawn sequentially, so a smaller ``n_tokens`` gives a prefix of a larger
-    draw from the same chunk.
+    x is the residual entering the FFN pre-norm: x_pre (the residual entering the
+    layer's attention pre-norm) plus the attention output.  With ``with_pre`` the stored
+    x_pre is returned as a third element; the down edge of layer i-1 reads it as the
+    residual entering layer i.  Rows are drawn sequentially, so a smaller ``n_tokens``
+    gives a prefix of a larger draw from the same chunk.
     """
     d = wl.d_model
     gx = _rng(wl, layer, 1, chunk)
@@ -166,6 +191,8 @@ def host_tokens(wl: Workload, layer: int, weights: LayerWeights, n_tokens: int,
     z = store(_heads(gz, wl, n_tokens), wl.dtype)
     z64 = to_f64(z).reshape(n_tokens, wl.attn_width)
     x = x_pre + z64 @ to_f64(weights.w_o).T
+    if with_pre:
+        return store(x, wl.dtype), z, store(x_pre, wl.dtype)
     return store(x, wl.dtype), z
 
 
@@ -194,7 +221,24 @@ def device_weights(wl: Workload, layer: int, device) -> dict:
     return out
 
 
-def device_tokens(wl: Workload, layer: int, weights: dict, n_tokens: int, chunk: int, device):
+def device_attn_weights(wl: Workload, layer: int, device) -> dict:
+    """Same recipe as ``host_attn_weights`` with torch's generator on ``device``."""
+    import torch
+    gen = torch.Generator(device=device)
+    gen.manual_seed(int(np.random.SeedSequence([SEED_ROOT, wl.key, layer, 0, 1]).generate_state(1)[0]))
+    dt = torch.bfloat16 if wl.dtype == "bf16" else torch.float32
+    d, HD, GD = wl.d_model, wl.attn_width, wl.n_kv_groups * wl.head_dim
+    s = wl.weight_std
+
+    def nrm(*shape):
+        return torch.randn(*shape, generator=gen, device=device, dtype=torch.float32)
+
+    return {"w_q": (nrm(HD, d) * s).to(dt), "w_k": (nrm(GD, d) * s).to(dt),
+            "w_v": (nrm(GD, d) * s).to(dt), "gamma": (1.0 + nrm(d) * wl.gamma_std).to(dt)}
+
+
+def device_tokens(wl: Workload, layer: int, weights: dict, n_tokens: int, chunk: int, device,
+                  with_pre: bool = False):
     """(x [T,d], attn [T,H,dh]) on ``device``, same recipe as ``host_tokens``."""
     import torch
     gen = torch.Generator(device=device)
@@ -214,5 +258,7 @@ def device_tokens(wl: Workload, layer: int, weights: dict, n_tokens: int, chunk:
         z = nrm / torch.sqrt(chi2 / 4.0)
     z = z.to(dt)
     x = x_pre + (z.reshape(n_tokens, -1).float() @ weights["w_o"].float().t())
+    if with_pre:
+        return x.to(dt).contiguous(), z.contiguous(), x_pre.to(dt).contiguous()
     return x.to(dt).contiguous(), z.contiguous()
 

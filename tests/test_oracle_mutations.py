@@ -84,3 +84,52 @@ def test_wrong_tie_break_is_caught(monkeypatch):
     monkeypatch.setattr(lay, "best_partition", lambda s, minimise=False: int(np.argmax(s[::-1]) * -1 + len(s) - 1))
     with pytest.raises(AssertionError):
         pl.test_head_step_brute_force_and_ties()
+
+
+# ----------------------------------------------------------------------------- down edge
+from oracle import down as dwn  # noqa: E402
+from tests import test_oracle_down as pd  # noqa: E402
+
+
+@pytest.fixture(scope="module")
+def tiny_down():
+    return pd._data()
+
+
+def test_down_gain_dropped_is_caught(tiny_down, monkeypatch):
+    orig = dwn.down_weight_norms
+
+    def bad(w_q, w_k, w_v, gamma_next, w_down, H, G):
+        return orig(w_q, w_k, w_v, np.ones_like(gamma_next), w_down, H, G)
+    monkeypatch.setattr(dwn, "down_weight_norms", bad)
+    with pytest.raises(AssertionError):
+        pd.test_equals_removal_through_next_projection(tiny_down)
+
+
+def test_down_wrong_rms_is_caught(tiny_down, monkeypatch):
+    orig = dwn.down_token_stat
+
+    def bad(x, gamma, w_gate, w_up, eps, x_next, eps_next):  # this layer's r instead of r'
+        return orig(x, gamma, w_gate, w_up, eps, x, eps)
+    monkeypatch.setattr(dwn, "down_token_stat", bad)
+    with pytest.raises(AssertionError):
+        pd.test_equals_removal_through_next_projection(tiny_down)
+
+
+def test_down_wrong_group_rows_are_caught(tiny_down, monkeypatch):
+    def bad(H, G, dh, g):  # strided query heads instead of consecutive ones
+        q = np.concatenate([np.arange(h * dh, (h + 1) * dh) for h in range(g, H, G)])
+        return q, np.arange(g * dh, (g + 1) * dh)
+    monkeypatch.setattr(dwn, "qkv_rows", bad)
+    with pytest.raises(AssertionError):
+        pd.test_equals_removal_through_next_projection(tiny_down)
+
+
+def test_down_value_rows_dropped_are_caught(tiny_down, monkeypatch):
+    def bad(w_q, w_k, w_v, H, G, g):
+        dh = w_k.shape[0] // G
+        q, kv = dwn.qkv_rows(H, G, dh, g)
+        return np.concatenate([w_q[q], w_k[kv]], axis=0)
+    monkeypatch.setattr(dwn, "group_projection", bad)
+    with pytest.raises(AssertionError):
+        pd.test_equals_removal_through_next_projection(tiny_down)
