@@ -88,6 +88,43 @@ dtp_status dtp_layer_set_weights(dtp_layer layer, const void* w_o, const void* g
 dtp_status dtp_affinity_accumulate(dtp_layer layer, const void* x, const void* attn,
                                    int64_t n_tokens, float* A, void* stream);
 
+/* The same accumulation of A, plus the token statistic of the down edge (Section 3,
+ * "Affinity scores", down edge) in the same pass:
+ *   s_down[k] += sum_t alpha_k(t)^2 / r'_t^2,  alpha_k = silu(g_k) u_k,
+ *   r'_t = sqrt(mean(x_next[t]^2) + rms_eps_next),
+ * with g_k, u_k at the layer's operating point and x_next the residual entering the next
+ * layer's attention pre-norm (held fixed, as r is).
+ *   x_next dev [n_tokens, d]  layer dtype, 16-byte aligned
+ *   s_down dev [I] float       accumulated in place (+=); deterministic for fixed shapes
+ * x_next and s_down are both required (DTP_ERR_INVALID_ARG otherwise). */
+dtp_status dtp_affinity_accumulate_down(dtp_layer layer, const void* x, const void* attn,
+                                        const void* x_next, float rms_eps_next,
+                                        int64_t n_tokens, float* A, float* s_down,
+                                        void* stream);
+
+/* Weight-only factor of the down edge into the next layer (Section 3, down edge):
+ *   B[g, k] = || W^{qkv}_g (gamma' * w^d_k) ||^2,
+ * W^{qkv}_g the q rows of next-layer KV group g's query heads (consecutive heads share a
+ * group), then its k rows and v rows; gamma' the next layer's attention pre-norm gain;
+ * w^d_k column k of this layer's W_down.  Sizes are the next layer's heads and this
+ * layer's d and I.
+ *   w_q dev [H*dh, d], w_k / w_v dev [G*dh, d]  (q_proj/k_proj/v_proj.weight layouts)
+ *   gamma_next dev [d], w_down dev [d, I]       all in `dtype`, 16-byte aligned
+ *   B dev [G, I] float                          written
+ * bf16: MFMA over d with gamma' * w^d_k rounded to bf16, fp32 sums of squares; requires
+ * d and I multiples of 8.  f32: plain FMAs (small shapes).  Scratch of G*I*ceil((H/G+2)*dh
+ * /128) floats is taken from the stream-ordered allocator and returned before exit. */
+dtp_status dtp_down_weights(int32_t d_model, int32_t n_neurons, int32_t n_q_heads,
+                            int32_t n_kv_groups, int32_t head_dim, dtp_dtype dtype,
+                            const void* w_q, const void* w_k, const void* w_v,
+                            const void* gamma_next, const void* w_down, float* B, void* stream);
+
+/* Raw down affinity S_down[k, g] = s_down[k] * B[g, k] (the A_down operand of
+ * dtp_coordinate_ascent for this layer).
+ *   s_down dev [I], B dev [G, I], A_down dev [I, G] float (written). */
+dtp_status dtp_down_affinity(int32_t n_neurons, int32_t n_kv_groups, const float* s_down,
+                             const float* B, float* A_down, void* stream);
+
 /* Timing of the affinity kernel with HIP events on the launch stream.  After
  * dtp_layer_profile(layer, 1), every accumulate call records an event pair around each
  * launch of its dominant kernel; dtp_layer_profile_read synchronises those events and

@@ -33,13 +33,10 @@
 #include <vector>
 
 #include "dtp_internal.h"
+#include "tile_mfma.h"
 
 namespace dtp {
 namespace {
-
-typedef __attribute__((ext_vector_type(8))) __bf16 bf16x8;
-typedef __attribute__((ext_vector_type(16))) float f32x16;
-typedef __attribute__((ext_vector_type(4))) uint32_t u32x4;
 
 constexpr int kBM = 128;          // tokens per block tile: 4 waves x 32 rows
 constexpr int kBN = 64;           // neurons per block tile
@@ -52,82 +49,12 @@ constexpr int kMaxSplits = 128;        // token splits per launch (size of the p
 constexpr int kTileTokens = 1 << 15;   // tokens per bf16 slice (size of the tiled token buffer)
 constexpr int kTargetBlocks = 3072;    // aim for this many blocks per launch
 
-__device__ inline float bf16_to_f32(uint16_t b) { return __uint_as_float((uint32_t)b << 16); }
-
-__device__ inline uint16_t f32_to_bf16(float f) {
-  uint32_t u = __float_as_uint(f);
-  if ((u & 0x7fffffffu) > 0x7f800000u) return 0x7fc0;  // NaN stays NaN
-  u += 0x7fffu + ((u >> 16) & 1u);                      // round to nearest even
-  return (uint16_t)(u >> 16);
-}
-
 template <typename T>
 __device__ inline float load_f32(const T* p, int64_t i);
 template <>
 __device__ inline float load_f32<uint16_t>(const uint16_t* p, int64_t i) { return bf16_to_f32(p[i]); }
 template <>
 __device__ inline float load_f32<float>(const float* p, int64_t i) { return p[i]; }
-
-// ------------------------------------------------------------------ tile staging (bf16)
-// A stage is 128 rows x KC contraction columns; each of the 256 threads moves KC/16
-// segments of 16 bytes (8 bf16) from global memory into registers, then into LDS.
-template <int KC>
-struct Stage {
-  u32x4 v[KC / 16];
-};
-
-template <int KC>
-__device__ inline void stage_load(Stage<KC>& s, const uint16_t* __restrict__ base, int64_t ld,
-                                  int rows_valid, int k0, int k_valid) {
-  constexpr int kSegs = KC / 8;              // 16-byte segments per row
-  constexpr int kRowsPerPass = kThreads / kSegs;
-  const int t = threadIdx.x;
-  const int k = k0 + (t % kSegs) * 8;
-#pragma unroll
-  for (int j = 0; j < KC / 16; ++j) {
-    const int row = t / kSegs + kRowsPerPass * j;
-    if (row < rows_valid && k < k_valid)
-      s.v[j] = *reinterpret_cast<const u32x4*>(base + (int64_t)row * ld + k);
-    else
-      s.v[j] = u32x4{0u, 0u, 0u, 0u};
-  }
-}
-
-template <int KC>
-__device__ inline void stage_store(const Stage<KC>& s, uint16_t* lds) {
-  constexpr int kSegs = KC / 8;
-  constexpr int kRowsPerPass = kThreads / kSegs;
-  const int t = threadIdx.x;
-#pragma unroll
-  for (int j = 0; j < KC / 16; ++j) {
-    const int row = t / kSegs + kRowsPerPass * j;
-    *reinterpret_cast<u32x4*>(lds + row * (KC + 8) + (t % kSegs) * 8) = s.v[j];
-  }
-}
-
-// One stage of MFMA work: the wave's 32 rows of A against the 128 columns of B, with LDS
-// rows of KC + 8 bf16 (the 16 bytes of padding spread consecutive rows over the banks).
-// v_mfma_f32_32x32x16_bf16: lane l feeds row (l % 32) of A / column (l % 32) of B with the
-// 8 contraction elements starting at 8 * (l / 32).
-template <int KC>
-__device__ inline void mfma_stage(const uint16_t* As, const uint16_t* Bs, f32x16 (&acc)[4],
-                                  int wave, int lane) {
-  constexpr int kRow = KC + 8;
-  const int r = lane & 31;
-  const int kh = (lane >> 5) * 8;
-#pragma unroll
-  for (int ks = 0; ks < KC; ks += 16) {
-    const bf16x8 a = *reinterpret_cast<const bf16x8*>(As + (wave * 32 + r) * kRow + ks + kh);
-#pragma unroll
-    for (int b = 0; b < 4; ++b) {
-      const bf16x8 bb = *reinterpret_cast<const bf16x8*>(Bs + (b * 32 + r) * kRow + ks + kh);
-      acc[b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, bb, acc[b], 0, 0, 0);
-    }
-  }
-}
-
-// Row (within the wave's 32) held by accumulator element i of lane l.
-__device__ inline int acc_row(int i, int lane) { return 8 * (i >> 2) + 4 * (lane >> 5) + (i & 3); }
 
 // ------------------------------------------------------------------ weight preparation
 // out[tile*128 + c][j] (row stride ld) = W[k][j] * gamma[j], k = tile*64 + c%64,
@@ -352,8 +279,9 @@ struct AffinityArgs {
   const uint16_t* xt;     // token rows [x | attn] in the tiled layout of tile_tokens_kernel
   const uint16_t* wcat;   // [n_tiles*128][Kt], Kt = d + H*dh
   const float* rinv;      // [T]
+  const float* rinv_next; // [T] 1/r' of the residual entering the next layer, or NULL
   const float* nd;        // [I_pad]
-  float* partial;         // [splits][G][I_pad]
+  float* partial;         // [splits][G+1][I_pad]: G up rows, then the down statistic
   int T, d, H, G, dh, n_tiles, splits, I_pad, Kt, nrb;  // nrb: 32-row blocks in xt
 };
 
@@ -535,14 +463,17 @@ affinity_bf16_kernel(AffinityArgs p) {
   using WStage = WeightStage<KC, kStageCols, NT>;
   __shared__ __attribute__((aligned(16))) uint16_t Bs[2][kStageCols * (KC + 8)];
   __shared__ __attribute__((aligned(16))) float rv[kRows];  // 1/r of the tile's rows, 0 past T
-  extern __shared__ float red[];  // [WM*WN][G][32*NB]
+  __shared__ __attribute__((aligned(16))) float rv2[kRows];  // 1/r' of the rows (down statistic)
+  extern __shared__ float red[];  // [WM*WN][G+1][32*NB]
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int wm = wave % WM, wn = wave / WM;
   int tg, split;  // neuron group and token split of this block
   block_work<SG>(blockIdx.x, (int)gridDim.x / p.splits, p.splits, tg, split);
   const int hpg = p.H / p.G;
 
-  for (int i = threadIdx.x; i < WM * WN * p.G * 32 * NB; i += NT) red[i] = 0.0f;
+  const int G1 = p.G + 1;  // banked rows: the G up groups, then the down statistic
+  const bool down = p.rinv_next != nullptr;
+  for (int i = threadIdx.x; i < WM * WN * G1 * 32 * NB; i += NT) red[i] = 0.0f;
 
   const int mtiles = (p.T + kRows - 1) / kRows;
   const int per = (mtiles + p.splits - 1) / p.splits;
@@ -592,7 +523,10 @@ affinity_bf16_kernel(AffinityArgs p) {
     load_tokens_for(t1, min(1, nq - 1));
     load_weights(w1, w_tile, p.Kt, min(1, nq - 1) * KC);
     store_weights(w0, Bs[0]);
-    for (int i = threadIdx.x; i < kRows; i += NT) rv[i] = m0 + i < p.T ? p.rinv[m0 + i] : 0.0f;
+    for (int i = threadIdx.x; i < kRows; i += NT) {
+      rv[i] = m0 + i < p.T ? p.rinv[m0 + i] : 0.0f;
+      rv2[i] = down && m0 + i < p.T ? p.rinv_next[m0 + i] : 0.0f;
+    }
     __syncthreads();
 
     // Stage q: tokens in `cur`, stage q+1's weights in `wnext` (stored to LDS here),
@@ -632,6 +566,34 @@ affinity_bf16_kernel(AffinityArgs p) {
               }
             }
           }
+        if (down) {
+          // Down-edge statistic: (alpha / r')^2 with alpha = silu(g) u, summed over rows.
+          float ds[NB];
+#pragma unroll
+          for (int nb = 0; nb < NB; ++nb) ds[nb] = 0.0f;
+#pragma unroll
+          for (int rb = 0; rb < RB; ++rb)
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+              const int row = 32 * (RB * wm + rb) + 8 * j + 4 * (lane >> 5);
+              const float4 r4 = *reinterpret_cast<const float4*>(rv + row);
+              const float4 n4 = *reinterpret_cast<const float4*>(rv2 + row);
+#pragma unroll
+              for (int k = 0; k < 4; ++k)
+#pragma unroll
+                for (int nb = 0; nb < NB; ++nb) {
+                  const float g = acc[rb][nb][0][4 * j + k] * r4[k];
+                  const float u = acc[rb][nb][1][4 * j + k] * r4[k];
+                  const float a = g * __builtin_amdgcn_rcpf(1.0f + __expf(-g)) * u * n4[k];
+                  ds[nb] = fmaf(a, a, ds[nb]);
+                }
+            }
+#pragma unroll
+          for (int nb = 0; nb < NB; ++nb) {
+            const float t = ds[nb] + __shfl_xor(ds[nb], 32, 64);
+            if (lane < 32) red[(wave * G1 + p.G) * (32 * NB) + 32 * nb + lane] += t;
+          }
+        }
       } else if (q >= nq1 && ++head_stage == nqh) {
         // Head h done: Delta = c1 (a_h . Fg) + c2 (a_h . Fu); sum Delta^2 over the rows.
 #pragma unroll
@@ -649,7 +611,7 @@ affinity_bf16_kernel(AffinityArgs p) {
 #pragma unroll
           for (int nb = 0; nb < NB; ++nb) {
             const float t = colsum[nb] + __shfl_xor(colsum[nb], 32, 64);
-            if (lane < 32) red[(wave * p.G + h / hpg) * (32 * NB) + 32 * nb + lane] += t;
+            if (lane < 32) red[(wave * G1 + h / hpg) * (32 * NB) + 32 * nb + lane] += t;
             colsum[nb] = 0.0f;
           }
         }
@@ -677,13 +639,13 @@ affinity_bf16_kernel(AffinityArgs p) {
   }
 
   // Sum the row waves in a fixed order and scale by ||w^d_k||^2.
-  for (int i = threadIdx.x; i < p.G * kNeurons; i += NT) {
+  for (int i = threadIdx.x; i < G1 * kNeurons; i += NT) {
     const int g = i / kNeurons, nl = i % kNeurons;
     const int cw = nl / (32 * NB), k = nl % (32 * NB);
     float sum = 0.0f;
-    for (int w = 0; w < WM; ++w) sum += red[((cw * WM + w) * p.G + g) * (32 * NB) + k];
+    for (int w = 0; w < WM; ++w) sum += red[((cw * WM + w) * G1 + g) * (32 * NB) + k];
     const int n = tg * kNeurons + nl;
-    p.partial[((int64_t)split * p.G + g) * p.I_pad + n] = sum * p.nd[n];
+    p.partial[((int64_t)split * G1 + g) * p.I_pad + n] = g < p.G ? sum * p.nd[n] : sum;
   }
 }
 
@@ -695,7 +657,10 @@ int launch_affinity(AffinityArgs p, hipStream_t s) {
   const int groups = p.n_tiles * kBN / kNeurons;
   const int mtiles = (p.T + kRows - 1) / kRows;
   p.splits = std::max(1, std::min((kTargetBlocks + groups - 1) / groups, std::min(mtiles, kMaxSplits)));
-  const size_t shm = sizeof(float) * WM * WN * p.G * 32 * NB;
+  const size_t shm = sizeof(float) * WM * WN * (p.G + 1) * 32 * NB;
+  if (shm > 65536)  // beyond the default dynamic LDS limit (G close to 32)
+    (void)hipFuncSetAttribute((const void*)&affinity_bf16_kernel<KC, WM, WN, RB, NB, PACK, SG>,
+                              hipFuncAttributeMaxDynamicSharedMemorySize, (int)shm);
   affinity_bf16_kernel<KC, WM, WN, RB, NB, PACK, SG><<<groups * p.splits, 64 * WM * WN, shm, s>>>(p);
   return p.splits;
 }
@@ -708,23 +673,24 @@ struct AffinityF32Args {
   const float* wgu;    // [n_tiles*128][d] gamma-scaled gate | up rows per tile
   const float* fold;   // [H][2][I][dh]
   const float* rinv;
+  const float* rinv_next;  // or NULL
   const float* nd;
-  float* partial;      // [splits][G][I_pad]
+  float* partial;      // [splits][G+1][I_pad]
   int T, d, H, G, dh, I, I_pad, splits;
 };
 
 __global__ void __launch_bounds__(256)
 affinity_f32_kernel(AffinityF32Args p) {
   // blockDim = 256 = 4 token lanes x 64 neurons of one tile
-  __shared__ float red[4][kMaxAffinityGroups][kBN];
+  __shared__ float red[4][kMaxAffinityGroups + 1][kBN];
   const int kl = threadIdx.x & 63, tl = threadIdx.x >> 6;
   const int tile = blockIdx.x / p.splits, split = blockIdx.x % p.splits;
   const int k = tile * kBN + kl;
   const int HD = p.H * p.dh, hpg = p.H / p.G;
   const int per = (p.T + p.splits - 1) / p.splits;
   const int t0 = split * per, t1 = min(p.T, t0 + per);
-  float acc[kMaxAffinityGroups];
-  for (int g = 0; g < p.G; ++g) acc[g] = 0.0f;
+  float acc[kMaxAffinityGroups + 1];
+  for (int g = 0; g <= p.G; ++g) acc[g] = 0.0f;
   if (k < p.I) {
     const float* wg = p.wgu + (int64_t)tile * kCols * p.d + (int64_t)kl * p.d;
     const float* wu = wg + (int64_t)kBN * p.d;
@@ -739,6 +705,10 @@ affinity_f32_kernel(AffinityF32Args p) {
       g *= ri;
       u *= ri;
       const float sg = 1.0f / (1.0f + expf(-g));
+      if (p.rinv_next) {
+        const float a = g * sg * u * p.rinv_next[t];
+        acc[p.G] = fmaf(a, a, acc[p.G]);
+      }
       const float cc2 = g * sg * ri;
       const float cc1 = sg * (1.0f + g * (1.0f - sg)) * u * ri;
       for (int h = 0; h < p.H; ++h) {
@@ -755,25 +725,29 @@ affinity_f32_kernel(AffinityF32Args p) {
       }
     }
   }
-  for (int g = 0; g < p.G; ++g) red[tl][g][kl] = acc[g];
+  for (int g = 0; g <= p.G; ++g) red[tl][g][kl] = acc[g];
   __syncthreads();
-  for (int i = threadIdx.x; i < p.G * kBN; i += 256) {
+  for (int i = threadIdx.x; i < (p.G + 1) * kBN; i += 256) {
     const int g = i / kBN, kk = i % kBN;
     const float s = red[0][g][kk] + red[1][g][kk] + red[2][g][kk] + red[3][g][kk];
     const int n = tile * kBN + kk;
-    p.partial[((int64_t)split * p.G + g) * p.I_pad + n] = s * p.nd[n];
+    p.partial[((int64_t)split * (p.G + 1) + g) * p.I_pad + n] = g < p.G ? s * p.nd[n] : s;
   }
 }
 
-// A[g][k] += sum_s partial[s][g][k], in fp64 and in split order.
+// A[g][k] += sum_s partial[s][g][k] for g < G, and s_down[k] += sum_s partial[s][G][k] when
+// s_down is given, in fp64 and in split order.
 __global__ void reduce_splits_kernel(const float* __restrict__ partial, int splits, int G, int I,
-                                     int I_pad, float* __restrict__ A) {
+                                     int I_pad, float* __restrict__ A, float* __restrict__ s_down) {
   const int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (idx >= (int64_t)G * I) return;
+  const int rows = s_down ? G + 1 : G;
+  if (idx >= (int64_t)rows * I) return;
   const int g = (int)(idx / I), k = (int)(idx % I);
-  double s = (double)A[idx];
-  for (int sp = 0; sp < splits; ++sp) s += (double)partial[((int64_t)sp * G + g) * I_pad + k];
-  A[idx] = (float)s;
+  float* out = g < G ? A + idx : s_down + k;
+  double s = (double)*out;
+  for (int sp = 0; sp < splits; ++sp)
+    s += (double)partial[((int64_t)sp * (G + 1) + g) * I_pad + k];
+  *out = (float)s;
 }
 
 inline unsigned grid_for(int64_t n, int threads) {
@@ -798,6 +772,7 @@ struct dtp_layer_s {
   float* fold32 = nullptr;   // f32 path: [H][2][I][dh]
   float* nd = nullptr;       // [I_pad]
   float* rinv = nullptr;     // [kSliceTokens]
+  float* rinv_next = nullptr;  // [kSliceTokens], 1/r' for the down statistic
   float* partial = nullptr;  // [kMaxSplits][G][I_pad]
   uint16_t* xt = nullptr;    // bf16 path: one slice of tiled token rows
   int64_t tile_slice = 0;    // tokens per bf16 slice
@@ -808,7 +783,7 @@ struct dtp_layer_s {
 namespace {
 
 void layer_free(dtp_layer L) {
-  void* bufs[] = {L->w, L->woT, L->fold32, L->nd, L->rinv, L->partial, L->xt};
+  void* bufs[] = {L->w, L->woT, L->fold32, L->nd, L->rinv, L->rinv_next, L->partial, L->xt};
   for (void* b : bufs)
     if (b) (void)hipFree(b);
   for (auto& e : L->events) {
@@ -827,6 +802,143 @@ dtp_status check_device(dtp_layer L) {
 }
 
 }  // namespace
+
+namespace dtp {
+namespace {
+
+// Shared body of the two accumulate entry points; x_next / s_down are NULL for the up
+// affinity alone.
+dtp_status accumulate(dtp_layer L, const void* x, const void* attn, const void* x_next,
+                      float eps_next, int64_t n_tokens, float* A, float* s_down, void* stream) {
+  DTP_CHECK(L != nullptr, DTP_ERR_INVALID_ARG, "layer is NULL");
+  DTP_CHECK(n_tokens >= 0, DTP_ERR_INVALID_ARG, "n_tokens=%lld is negative", (long long)n_tokens);
+  if (n_tokens == 0) return DTP_OK;
+  DTP_CHECK(x && attn && A, DTP_ERR_INVALID_ARG, "x, attn or A is NULL");
+  DTP_CHECK(aligned16(x) && aligned16(attn), DTP_ERR_INVALID_ARG,
+            "x and attn must be 16-byte aligned");
+  DTP_CHECK((x_next == nullptr) == (s_down == nullptr), DTP_ERR_INVALID_ARG,
+            "x_next and s_down must be given together");
+  DTP_CHECK(x_next == nullptr || aligned16(x_next), DTP_ERR_INVALID_ARG,
+            "x_next must be 16-byte aligned");
+  DTP_CHECK(std::isfinite(eps_next) && eps_next >= 0.0f, DTP_ERR_INVALID_ARG,
+            "rms_eps_next=%g must be finite and >= 0", (double)eps_next);
+  DTP_CHECK(L->has_weights, DTP_ERR_INVALID_ARG, "dtp_layer_set_weights was not called");
+  dtp_status st = check_device(L);
+  if (st != DTP_OK) return st;
+  hipStream_t s = (hipStream_t)stream;
+  const dtp_layer_desc& d = L->desc;
+  const int H = d.n_q_heads, dh = d.head_dim, HD = H * dh, G = d.n_kv_groups;
+  const int I = d.n_neurons, dm = d.d_model;
+  const size_t esz = d.dtype == DTP_BF16 ? 2 : 4;
+  // Tokens per slice: the 1/r buffer size, and element offsets of a slice below 2^30.
+  const int64_t width = std::max(dm, HD);
+  int64_t slice = std::max<int64_t>(256, std::min<int64_t>(kSliceTokens, ((int64_t)1 << 30) / width) / 256 * 256);
+  if (d.dtype == DTP_BF16) slice = std::min(slice, L->tile_slice);
+  for (int64_t t0 = 0; t0 < n_tokens; t0 += slice) {
+    const int T = (int)std::min<int64_t>(slice, n_tokens - t0);
+    const char* xs = (const char*)x + esz * (size_t)t0 * dm;
+    const char* as = (const char*)attn + esz * (size_t)t0 * HD;
+    const char* xns = x_next ? (const char*)x_next + esz * (size_t)t0 * dm : nullptr;
+    const unsigned rb = (unsigned)((T + 3) / 4);
+    if (d.dtype == DTP_BF16) {
+      rms_kernel<uint16_t><<<rb, 256, 0, s>>>((const uint16_t*)xs, T, dm, d.rms_eps, L->rinv);
+      if (xns)
+        rms_kernel<uint16_t><<<rb, 256, 0, s>>>((const uint16_t*)xns, T, dm, eps_next, L->rinv_next);
+    } else {
+      rms_kernel<float><<<rb, 256, 0, s>>>((const float*)xs, T, dm, d.rms_eps, L->rinv);
+      if (xns)
+        rms_kernel<float><<<rb, 256, 0, s>>>((const float*)xns, T, dm, eps_next, L->rinv_next);
+    }
+    DTP_HIP(hipGetLastError());
+    const float* rinv_next = xns ? L->rinv_next : nullptr;
+    // bf16: rewrite the slice's token rows into the fragment-contiguous layout.  Stages
+    // are as deep as the operating point and the heads both divide.
+    const int kc = dm % 64 == 0 && dh % 64 == 0 ? 64 : dm % 32 == 0 && dh % 32 == 0 ? 32 : 16;
+    const int nrb = (T + 31) / 32;
+    if (d.dtype == DTP_BF16) {
+      const int64_t n_chunks = (int64_t)nrb * 32 * L->Kt / 8;
+      const unsigned tgrid = (unsigned)((n_chunks + 255) / 256);
+      if (kc == 64)
+        tile_tokens_kernel<64><<<tgrid, 256, 0, s>>>((const uint16_t*)xs, (const uint16_t*)as, L->rinv, T,
+                                                     dm, HD, L->Kt / kc, n_chunks, L->xt);
+      else if (kc == 32)
+        tile_tokens_kernel<32><<<tgrid, 256, 0, s>>>((const uint16_t*)xs, (const uint16_t*)as, L->rinv, T,
+                                                     dm, HD, L->Kt / kc, n_chunks, L->xt);
+      else
+        tile_tokens_kernel<16><<<tgrid, 256, 0, s>>>((const uint16_t*)xs, (const uint16_t*)as, L->rinv, T,
+                                                     dm, HD, L->Kt / kc, n_chunks, L->xt);
+      DTP_HIP(hipGetLastError());
+    }
+
+    int splits;
+    hipEvent_t e0 = nullptr, e1 = nullptr;
+    if (L->profiling) {
+      DTP_HIP(hipEventCreate(&e0));
+      DTP_HIP(hipEventCreate(&e1));
+      DTP_HIP(hipEventRecord(e0, s));
+    }
+    if (d.dtype == DTP_BF16) {
+      AffinityArgs p;
+      p.xt = L->xt;
+      p.wcat = (const uint16_t*)L->w;
+      p.rinv = L->rinv;
+      p.rinv_next = rinv_next;
+      p.nd = L->nd;
+      p.partial = L->partial;
+      p.T = T;
+      p.d = dm;
+      p.H = H;
+      p.G = G;
+      p.dh = dh;
+      p.n_tiles = L->n_tiles;
+      p.I_pad = L->I_pad;
+      p.Kt = L->Kt;
+      p.nrb = nrb;
+      p.splits = 0;
+      // Eight wavefronts per block (one block per CU): 256 tokens x 64 neurons per tile;
+      // four for 16-wide stages, whose weight stage has only 256 16-byte pieces.
+      if (kc == 64)
+        splits = launch_affinity<64, 8, 1, 1, 2, true>(p, s);
+      else if (kc == 32)
+        splits = launch_affinity<32, 8, 1, 1, 2, true>(p, s);
+      else
+        splits = launch_affinity<16, 4, 1, 1, 2, true>(p, s);
+    } else {
+      splits = (kTargetBlocks / 4 + L->n_tiles - 1) / L->n_tiles;
+      splits = std::max(1, std::min(splits, std::min(T, kMaxSplits)));
+      AffinityF32Args p;
+      p.x = (const float*)xs;
+      p.attn = (const float*)as;
+      p.wgu = (const float*)L->w;
+      p.fold = L->fold32;
+      p.rinv = L->rinv;
+      p.rinv_next = rinv_next;
+      p.nd = L->nd;
+      p.partial = L->partial;
+      p.T = T;
+      p.d = dm;
+      p.H = H;
+      p.G = G;
+      p.dh = dh;
+      p.I = I;
+      p.I_pad = L->I_pad;
+      p.splits = splits;
+      affinity_f32_kernel<<<L->n_tiles * splits, 256, 0, s>>>(p);
+    }
+    DTP_HIP(hipGetLastError());
+    if (L->profiling) {
+      DTP_HIP(hipEventRecord(e1, s));
+      L->events.emplace_back(e0, e1);
+    }
+    reduce_splits_kernel<<<grid_for((int64_t)(G + 1) * I, 256), 256, 0, s>>>(
+        L->partial, splits, G, I, L->I_pad, A, s_down);
+    DTP_HIP(hipGetLastError());
+  }
+  return DTP_OK;
+}
+
+}  // namespace
+}  // namespace dtp
 
 extern "C" {
 
@@ -876,7 +988,8 @@ dtp_status dtp_layer_create(const dtp_layer_desc* desc, dtp_layer* out) {
   if (e == hipSuccess) e = hipMalloc(&L->nd, 4 * (size_t)L->I_pad);
   if (e == hipSuccess) e = hipMalloc(&L->rinv, 4 * (size_t)kSliceTokens);
   if (e == hipSuccess)
-    e = hipMalloc(&L->partial, 4 * (size_t)kMaxSplits * d.n_kv_groups * L->I_pad);
+    e = hipMalloc(&L->partial, 4 * (size_t)kMaxSplits * (d.n_kv_groups + 1) * L->I_pad);
+  if (e == hipSuccess) e = hipMalloc(&L->rinv_next, 4 * (size_t)kSliceTokens);
   if (e != hipSuccess) {
     layer_free(L);
     return fail(e == hipErrorOutOfMemory ? DTP_ERR_NO_MEMORY : DTP_ERR_HIP,
@@ -940,116 +1053,15 @@ dtp_status dtp_layer_set_weights(dtp_layer L, const void* w_o, const void* gamma
 dtp_status dtp_affinity_accumulate(dtp_layer L, const void* x, const void* attn, int64_t n_tokens,
                                    float* A, void* stream) {
   clear_error();
-  DTP_CHECK(L != nullptr, DTP_ERR_INVALID_ARG, "layer is NULL");
-  DTP_CHECK(n_tokens >= 0, DTP_ERR_INVALID_ARG, "n_tokens=%lld is negative", (long long)n_tokens);
-  if (n_tokens == 0) return DTP_OK;
-  DTP_CHECK(x && attn && A, DTP_ERR_INVALID_ARG, "x, attn or A is NULL");
-  DTP_CHECK(aligned16(x) && aligned16(attn), DTP_ERR_INVALID_ARG,
-            "x and attn must be 16-byte aligned");
-  DTP_CHECK(L->has_weights, DTP_ERR_INVALID_ARG, "dtp_layer_set_weights was not called");
-  dtp_status st = check_device(L);
-  if (st != DTP_OK) return st;
-  hipStream_t s = (hipStream_t)stream;
-  const dtp_layer_desc& d = L->desc;
-  const int H = d.n_q_heads, dh = d.head_dim, HD = H * dh, G = d.n_kv_groups;
-  const int I = d.n_neurons, dm = d.d_model;
-  const size_t esz = d.dtype == DTP_BF16 ? 2 : 4;
-  // Tokens per slice: the 1/r buffer size, and element offsets of a slice below 2^30.
-  const int64_t width = std::max(dm, HD);
-  int64_t slice = std::max<int64_t>(256, std::min<int64_t>(kSliceTokens, ((int64_t)1 << 30) / width) / 256 * 256);
-  if (d.dtype == DTP_BF16) slice = std::min(slice, L->tile_slice);
-  for (int64_t t0 = 0; t0 < n_tokens; t0 += slice) {
-    const int T = (int)std::min<int64_t>(slice, n_tokens - t0);
-    const char* xs = (const char*)x + esz * (size_t)t0 * dm;
-    const char* as = (const char*)attn + esz * (size_t)t0 * HD;
-    const unsigned rb = (unsigned)((T + 3) / 4);
-    if (d.dtype == DTP_BF16)
-      rms_kernel<uint16_t><<<rb, 256, 0, s>>>((const uint16_t*)xs, T, dm, d.rms_eps, L->rinv);
-    else
-      rms_kernel<float><<<rb, 256, 0, s>>>((const float*)xs, T, dm, d.rms_eps, L->rinv);
-    DTP_HIP(hipGetLastError());
-    // bf16: rewrite the slice's token rows into the fragment-contiguous layout.  Stages
-    // are as deep as the operating point and the heads both divide.
-    const int kc = dm % 64 == 0 && dh % 64 == 0 ? 64 : dm % 32 == 0 && dh % 32 == 0 ? 32 : 16;
-    const int nrb = (T + 31) / 32;
-    if (d.dtype == DTP_BF16) {
-      const int64_t n_chunks = (int64_t)nrb * 32 * L->Kt / 8;
-      const unsigned tgrid = (unsigned)((n_chunks + 255) / 256);
-      if (kc == 64)
-        tile_tokens_kernel<64><<<tgrid, 256, 0, s>>>((const uint16_t*)xs, (const uint16_t*)as, L->rinv, T,
-                                                     dm, HD, L->Kt / kc, n_chunks, L->xt);
-      else if (kc == 32)
-        tile_tokens_kernel<32><<<tgrid, 256, 0, s>>>((const uint16_t*)xs, (const uint16_t*)as, L->rinv, T,
-                                                     dm, HD, L->Kt / kc, n_chunks, L->xt);
-      else
-        tile_tokens_kernel<16><<<tgrid, 256, 0, s>>>((const uint16_t*)xs, (const uint16_t*)as, L->rinv, T,
-                                                     dm, HD, L->Kt / kc, n_chunks, L->xt);
-      DTP_HIP(hipGetLastError());
-    }
+  return dtp::accumulate(L, x, attn, nullptr, 0.0f, n_tokens, A, nullptr, stream);
+}
 
-    int splits;
-    hipEvent_t e0 = nullptr, e1 = nullptr;
-    if (L->profiling) {
-      DTP_HIP(hipEventCreate(&e0));
-      DTP_HIP(hipEventCreate(&e1));
-      DTP_HIP(hipEventRecord(e0, s));
-    }
-    if (d.dtype == DTP_BF16) {
-      AffinityArgs p;
-      p.xt = L->xt;
-      p.wcat = (const uint16_t*)L->w;
-      p.rinv = L->rinv;
-      p.nd = L->nd;
-      p.partial = L->partial;
-      p.T = T;
-      p.d = dm;
-      p.H = H;
-      p.G = G;
-      p.dh = dh;
-      p.n_tiles = L->n_tiles;
-      p.I_pad = L->I_pad;
-      p.Kt = L->Kt;
-      p.nrb = nrb;
-      p.splits = 0;
-      // Eight wavefronts per block (one block per CU): 256 tokens x 64 neurons per tile;
-      // four for 16-wide stages, whose weight stage has only 256 16-byte pieces.
-      if (kc == 64)
-        splits = launch_affinity<64, 8, 1, 1, 2, true>(p, s);
-      else if (kc == 32)
-        splits = launch_affinity<32, 8, 1, 1, 2, true>(p, s);
-      else
-        splits = launch_affinity<16, 4, 1, 1, 2, true>(p, s);
-    } else {
-      splits = (kTargetBlocks / 4 + L->n_tiles - 1) / L->n_tiles;
-      splits = std::max(1, std::min(splits, std::min(T, kMaxSplits)));
-      AffinityF32Args p;
-      p.x = (const float*)xs;
-      p.attn = (const float*)as;
-      p.wgu = (const float*)L->w;
-      p.fold = L->fold32;
-      p.rinv = L->rinv;
-      p.nd = L->nd;
-      p.partial = L->partial;
-      p.T = T;
-      p.d = dm;
-      p.H = H;
-      p.G = G;
-      p.dh = dh;
-      p.I = I;
-      p.I_pad = L->I_pad;
-      p.splits = splits;
-      affinity_f32_kernel<<<L->n_tiles * splits, 256, 0, s>>>(p);
-    }
-    DTP_HIP(hipGetLastError());
-    if (L->profiling) {
-      DTP_HIP(hipEventRecord(e1, s));
-      L->events.emplace_back(e0, e1);
-    }
-    reduce_splits_kernel<<<grid_for((int64_t)G * I, 256), 256, 0, s>>>(L->partial, splits, G, I,
-                                                                       L->I_pad, A);
-    DTP_HIP(hipGetLastError());
-  }
-  return DTP_OK;
+dtp_status dtp_affinity_accumulate_down(dtp_layer L, const void* x, const void* attn,
+                                        const void* x_next, float rms_eps_next, int64_t n_tokens,
+                                        float* A, float* s_down, void* stream) {
+  clear_error();
+  DTP_CHECK(x_next && s_down, DTP_ERR_INVALID_ARG, "x_next or s_down is NULL");
+  return dtp::accumulate(L, x, attn, x_next, rms_eps_next, n_tokens, A, s_down, stream);
 }
 
 dtp_status dtp_layer_profile(dtp_layer L, int32_t enable) {

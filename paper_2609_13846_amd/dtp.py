@@ -51,6 +51,9 @@ _SIGNATURES = {
     "dtp_layer_destroy": (_I32, [_P]),
     "dtp_layer_set_weights": (_I32, [_P, _P, _P, _P, _P, _P, _P]),
     "dtp_affinity_accumulate": (_I32, [_P, _P, _P, _I64, _P, _P]),
+    "dtp_affinity_accumulate_down": (_I32, [_P, _P, _P, _P, ctypes.c_float, _I64, _P, _P, _P]),
+    "dtp_down_weights": (_I32, [_I32, _I32, _I32, _I32, _I32, _I32, _P, _P, _P, _P, _P, _P, _P]),
+    "dtp_down_affinity": (_I32, [_I32, _I32, _P, _P, _P, _P]),
     "dtp_layer_profile": (_I32, [_P, _I32]),
     "dtp_layer_profile_read": (_I32, [_P, ctypes.POINTER(ctypes.c_double), ctypes.POINTER(_I64)]),
     "dtp_partition_count": (_I64, [_I32, _I32]),
@@ -143,6 +146,25 @@ def dtp_layer_set_weights(layer, w_o, gamma, w_gate, w_up, w_down, stream=None):
 def dtp_affinity_accumulate(layer, x, attn, n_tokens, A, stream=None):
     _check(lib().dtp_affinity_accumulate(layer, _ptr(x), _ptr(attn), int(n_tokens), _ptr(A),
                                          _stream(stream)))
+
+
+def dtp_affinity_accumulate_down(layer, x, attn, x_next, rms_eps_next, n_tokens, A, s_down,
+                                 stream=None):
+    _check(lib().dtp_affinity_accumulate_down(layer, _ptr(x), _ptr(attn), _ptr(x_next),
+                                              float(rms_eps_next), int(n_tokens), _ptr(A),
+                                              _ptr(s_down), _stream(stream)))
+
+
+def dtp_down_weights(d_model, n_neurons, n_q_heads, n_kv_groups, head_dim, dtype, w_q, w_k, w_v,
+                     gamma_next, w_down, B, stream=None):
+    _check(lib().dtp_down_weights(d_model, n_neurons, n_q_heads, n_kv_groups, head_dim, int(dtype),
+                                  _ptr(w_q), _ptr(w_k), _ptr(w_v), _ptr(gamma_next), _ptr(w_down),
+                                  _ptr(B), _stream(stream)))
+
+
+def dtp_down_affinity(n_neurons, n_kv_groups, s_down, B, A_down, stream=None):
+    _check(lib().dtp_down_affinity(n_neurons, n_kv_groups, _ptr(s_down), _ptr(B), _ptr(A_down),
+                                   _stream(stream)))
 
 
 def dtp_layer_profile(layer, enable):

@@ -42,6 +42,7 @@ def oracle(wl, w, x, a, neurons=None):
     ("qwen3-0.6b-layer", 200, dict(n_neurons=1000)),               # ragged neuron tile
     ("qwen3-0.6b-layer", 130, dict(n_q_heads=2, n_kv_groups=1)),    # one group
     ("qwen3-0.6b-layer", 129, dict(n_q_heads=8, n_kv_groups=8, head_dim=48)),  # H = G, dh % 32 = 16
+    ("qwen3-0.6b-layer", 100, dict(n_q_heads=32, n_kv_groups=32, head_dim=64)),  # G at its limit
     ("danube3-500m", 64, dict(d_model=272, n_neurons=192)),         # d % 32 = 16
 ])
 def test_affinity_matches_oracle(name, T, shape):

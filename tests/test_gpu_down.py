@@ -1,0 +1,161 @@
+"""GPU parity of the down edge (Section 3, down edge) against the fp64 oracle.
+
+The token statistic s_down comes out of the affinity pass (dtp_affinity_accumulate_down),
+the weight factor B from dtp_down_weights, and S_down = s * B from dtp_down_affinity.
+
+Tolerance.  The paper fixes none for S_down; it is derived from the arithmetic.  The
+operating point contracts x with W' = gamma * W rounded to bf16 (2^-9 relative per
+element), so g and u carry a relative error of up to kappa * 2^-9, kappa being the
+cancellation ratio sum_j |W'_kj n_j| / |g|, and alpha^2 doubles it.  On few tokens a
+neuron's statistic can be dominated by one cancelling token: an fp64 emulation of exactly
+that rounding differs from the exact oracle by up to 1.1e-2 on the shapes below (129-600
+tokens).  So s_down and S_down are held to 2e-2 relative on entries above 1e-3 of the
+maximum, and in addition to 1e-4 against that emulation, which shows the remaining
+difference is the operand rounding and nothing else.  B (bf16 gamma' * w^d_k, fp32 sums)
+is held to the up affinity's 1e-2.
+"""
+import numpy as np
+import pytest
+
+from oracle import affinity as orc_up
+from oracle import down as orc
+from paper_2609_13846_amd import dtp, synth
+from tests.helpers import assert_affinity_close, layer_for, oracle_inputs, torch_dev
+
+DOWN_REL_TOL = 2e-2
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+
+
+def _inputs(wl, T, neurons=None):
+    w = synth.host_weights(wl, 0)
+    x, a, _ = synth.host_tokens(wl, 0, w, T, with_pre=True)
+    wn = synth.host_weights(wl, 1)
+    _, _, x_next = synth.host_tokens(wl, 1, wn, T, with_pre=True)
+    an = synth.host_attn_weights(wl, 1)
+    return w, x, a, x_next, an
+
+
+def _gpu(wl, w, x, a, x_next, an, chunks=None):
+    """(A, s_down, B, S_down) from the library, plus A from the plain accumulate."""
+    T = x.shape[0]
+    G, I = wl.n_kv_groups, wl.n_neurons
+    layer = layer_for(wl)
+    try:
+        dw = [torch_dev(v) for v in (w.w_o, w.gamma, w.w_gate, w.w_up, w.w_down)]
+        dtp.dtp_layer_set_weights(layer, *dw)
+        dx, da, dxn = torch_dev(x), torch_dev(a), torch_dev(x_next)
+        A = torch.zeros(G, I, dtype=torch.float32, device="cuda")
+        s = torch.zeros(I, dtype=torch.float32, device="cuda")
+        bounds = [0]
+        for c in (chunks or [T]):
+            bounds.append(bounds[-1] + c)
+        for t0, t1 in zip(bounds, bounds[1:]):
+            dtp.dtp_affinity_accumulate_down(layer, dx[t0:t1], da[t0:t1], dxn[t0:t1], wl.rms_eps,
+                                             t1 - t0, A, s)
+        A_plain = torch.zeros(G, I, dtype=torch.float32, device="cuda")
+        for t0, t1 in zip(bounds, bounds[1:]):
+            dtp.dtp_affinity_accumulate(layer, dx[t0:t1], da[t0:t1], t1 - t0, A_plain)
+        B = torch.zeros(G, I, dtype=torch.float32, device="cuda")
+        dt = dtp.DTP_BF16 if wl.dtype == "bf16" else dtp.DTP_F32
+        dq, dk, dv, dg = (torch_dev(v) for v in (an.w_q, an.w_k, an.w_v, an.gamma))
+        dtp.dtp_down_weights(wl.d_model, I, wl.n_q_heads, G, wl.head_dim, dt, dq, dk, dv, dg,
+                             dw[4], B)
+        S = torch.empty(I, G, dtype=torch.float32, device="cuda")
+        dtp.dtp_down_affinity(I, G, s, B, S)
+        torch.cuda.synchronize()
+        return A.cpu().numpy(), s.cpu().numpy(), B.cpu().numpy(), S.cpu().numpy(), A_plain.cpu().numpy()
+    finally:
+        dtp.dtp_layer_destroy(layer)
+
+
+def _stat_with_bf16_operands(wl, w, x, x_next):
+    """s_down with the operating point's W' = gamma * W rounded to bf16, in fp64."""
+    f = synth.to_f64
+    wg = f(synth.round_to_bf16_bits(f(w.w_gate) * f(w.gamma)[None, :]))
+    wu = f(synth.round_to_bf16_bits(f(w.w_up) * f(w.gamma)[None, :]))
+    X = f(x)
+    r = orc_up.rms(X, wl.rms_eps)
+    g = X @ wg.T / r[:, None]
+    u = X @ wu.T / r[:, None]
+    rn = orc_up.rms(f(x_next), wl.rms_eps)
+    return np.sum((orc_up.silu(g) * u / rn[:, None]) ** 2, axis=0)
+
+
+def _oracle(wl, w, x, x_next, an):
+    f = synth.to_f64
+    kw = dict(x=f(x), gamma=f(w.gamma), w_gate=f(w.w_gate), w_up=f(w.w_up), eps=wl.rms_eps,
+              x_next=f(x_next), eps_next=wl.rms_eps)
+    s = orc.down_token_stat(**kw)
+    B = orc.down_weight_norms(f(an.w_q), f(an.w_k), f(an.w_v), f(an.gamma), f(w.w_down),
+                              wl.n_q_heads, wl.n_kv_groups)
+    return s, B
+
+
+CASES = [
+    ("tiny", dict(), 512, None),
+    ("tiny", dict(), 37, None),
+    ("qwen3-0.6b-layer", dict(), 300, None),
+    ("qwen3-0.6b-layer", dict(), 600, [256, 344]),
+    ("danube3-500m", dict(), 257, None),
+    ("qwen3-0.6b-layer", dict(d_model=272, n_neurons=1000), 129, None),
+]
+
+
+@pytest.mark.parametrize("name,over,T,chunks", CASES,
+                         ids=[f"{c[0]}-{c[2]}{'-' + str(c[1]) if c[1] else ''}" for c in CASES])
+def test_down_edge_matches_oracle(name, over, T, chunks):
+    wl = synth.shaped(synth.WORKLOADS[name], **over)
+    w, x, a, x_next, an = _inputs(wl, T)
+    A, s, B, S, A_plain = _gpu(wl, w, x, a, x_next, an, chunks)
+    s_ref, B_ref = _oracle(wl, w, x, x_next, an)
+    assert_affinity_close(s[None, :], s_ref[None, :], rel=DOWN_REL_TOL)
+    assert_affinity_close(B, B_ref)
+    assert_affinity_close(S, s_ref[:, None] * B_ref.T, rel=DOWN_REL_TOL)
+    if wl.dtype == "bf16":
+        s_emu = _stat_with_bf16_operands(wl, w, x, x_next)
+        assert_affinity_close(s[None, :], s_emu[None, :], rel=1e-4)
+    # the down statistic rides along without changing the up affinity
+    np.testing.assert_array_equal(A, A_plain)
+
+
+def test_up_affinity_still_matches_oracle_with_down_statistic():
+    wl = synth.WORKLOADS["qwen3-0.6b-layer"]
+    w, x, a, x_next, an = _inputs(wl, 200)
+    A, *_ = _gpu(wl, w, x, a, x_next, an)
+    neurons = [0, 1, 63, 64, 1000, 3071]
+    ref = orc_up.affinity_folded(**oracle_inputs(w, x, a), n_kv_groups=wl.n_kv_groups,
+                                 eps=wl.rms_eps, neurons=neurons)
+    assert_affinity_close(A[:, neurons], ref)
+
+
+def test_down_weights_8b_shape_sampled_neurons():
+    """B at the 8B-class shape (d = 4096, I = 14336, 32/8 heads): neurons sampled."""
+    wl = synth.WORKLOADS["8b-class-4layer"]
+    w = synth.host_weights(wl, 0)
+    an = synth.host_attn_weights(wl, 1)
+    B = torch.zeros(wl.n_kv_groups, wl.n_neurons, dtype=torch.float32, device="cuda")
+    dq, dk, dv, dg, dd = (torch_dev(v) for v in (an.w_q, an.w_k, an.w_v, an.gamma, w.w_down))
+    dtp.dtp_down_weights(wl.d_model, wl.n_neurons, wl.n_q_heads, wl.n_kv_groups, wl.head_dim,
+                         dtp.DTP_BF16, dq, dk, dv, dg, dd, B)
+    torch.cuda.synchronize()
+    sample = np.array([0, 1, 127, 128, 5000, 14335])
+    f = synth.to_f64
+    ref = orc.down_weight_norms(f(an.w_q), f(an.w_k), f(an.w_v), f(an.gamma),
+                                f(w.w_down)[:, sample], wl.n_q_heads, wl.n_kv_groups)
+    assert_affinity_close(B.cpu().numpy()[:, sample], ref)
+
+
+def test_down_requires_next_residual():
+    wl = synth.WORKLOADS["tiny"]
+    layer = layer_for(wl)
+    try:
+        x = torch.zeros(4, wl.d_model, device="cuda")
+        a = torch.zeros(4, wl.attn_width, device="cuda")
+        A = torch.zeros(wl.n_kv_groups, wl.n_neurons, device="cuda")
+        with pytest.raises(dtp.DtpError):
+            dtp.dtp_affinity_accumulate_down(layer, x, a, None, 1e-6, 4, A, A)
+    finally:
+        dtp.dtp_layer_destroy(layer)
