@@ -26,6 +26,10 @@ Readings where the paper is silent (each listed in the design notes):
 * the oracle returns the raw token sum A = sum_t (...) rather than the mean E_t; the
   1/T factor cancels in the unit-mass normalisation of the objective.
 
+The ADD score of the same section, E_t[(p_h . w^g_k)^2 + (p_h . w^u_k)^2] summed over
+the query heads of each KV group, ignores the operating point and the neuron's write
+(no ||w^d_k||^2 factor): ``affinity_add_literal`` and ``affinity_add_folded``.
+
 Two forms:
 
 * ``affinity_literal`` materialises every p_h in model space, exactly as written;
@@ -139,3 +143,41 @@ def affinity_folded(x, attn, w_o, gamma, w_gate, w_up, w_down, n_kv_groups, eps,
             acc[h] += np.sum(dlt * dlt, axis=0)
     return _aggregate(acc, w_down, n_kv_groups)
 
+
+
+def _group_sum(per_head, n_kv_groups):
+    """sum over the query heads of each group: [H, I] -> [G, I]."""
+    grp = group_of_head(per_head.shape[0], n_kv_groups)
+    out = np.zeros((n_kv_groups, per_head.shape[1]))
+    for h in range(per_head.shape[0]):
+        out[grp[h]] += per_head[h]
+    return out
+
+
+def affinity_add_literal(x, attn, w_o, gamma, w_gate, w_up, n_kv_groups, eps, block: int = 128):
+    """Raw ADD up affinity [G, I]: sum_t (p_h . w^g_k)^2 + (p_h . w^u_k)^2 per group."""
+    T, H, _ = attn.shape
+    acc = np.zeros((H, w_gate.shape[0]))
+    for t0 in range(0, T, block):
+        sl = slice(t0, min(T, t0 + block))
+        p = head_pieces(x[sl], attn[sl], w_o, gamma, eps)
+        acc += np.sum((p @ w_gate.T) ** 2 + (p @ w_up.T) ** 2, axis=0)
+    return _group_sum(acc, n_kv_groups)
+
+
+def affinity_add_folded(x, attn, w_o, gamma, w_gate, w_up, n_kv_groups, eps, block: int = 1024,
+                        neurons=None):
+    """Raw ADD up affinity via the fold; ``neurons`` restricts the columns."""
+    T, H, _ = attn.shape
+    if neurons is not None:
+        neurons = np.asarray(neurons)
+        w_gate, w_up = w_gate[neurons], w_up[neurons]
+    fg = fold(w_o, gamma, w_gate, H)
+    fu = fold(w_o, gamma, w_up, H)
+    acc = np.zeros((H, w_gate.shape[0]))
+    for t0 in range(0, T, block):
+        sl = slice(t0, min(T, t0 + block))
+        r = rms(x[sl], eps)[:, None]
+        for h in range(H):
+            acc[h] += np.sum((attn[sl, h, :] @ fg[h] / r) ** 2 + (attn[sl, h, :] @ fu[h] / r) ** 2, axis=0)
+    return _group_sum(acc, n_kv_groups)

@@ -299,3 +299,71 @@ def coordinate_ascent(Q_up: list, Q_down, L: int, max_sweeps: int = 64,
             break
         J_prev = J
     return hs, nus, objective(Q_up, Q_down, hs, nus), sweeps
+
+
+# ----------------------------------------------------------------------------- random layouts
+SPLITMIX_GAMMA = 0x9E3779B97F4A7C15
+_M64 = (1 << 64) - 1
+
+
+def splitmix64(seed: int, n: int) -> int:
+    """Output n (from 0) of SplitMix64 started from state ``seed``: the state advances by
+    the golden-ratio increment and each state is mixed by two xor-shift-multiply rounds
+    and a final xor-shift (Steele, Lea and Flood, OOPSLA 2014)."""
+    z = (seed + (n + 1) * SPLITMIX_GAMMA) & _M64
+    z = ((z ^ (z >> 30)) * 0xBF58476D1CE4E5B9) & _M64
+    z = ((z ^ (z >> 27)) * 0x94D049BB133111EB) & _M64
+    return z ^ (z >> 31)
+
+
+def _shuffle(labels, seed: int, counter: int):
+    """Fisher-Yates from the last position down; position j swaps with
+    floor(r (j + 1) / 2^64) for the next generator output r.  Returns (labels, counter)."""
+    a = list(labels)
+    for j in range(len(a) - 1, 0, -1):
+        r = splitmix64(seed, counter)
+        counter += 1
+        i = (r * (j + 1)) >> 64
+        a[j], a[i] = a[i], a[j]
+    return a, counter
+
+
+def random_layout(N: int, G: int, I: int, L: int, seed: int):
+    """Seeded balanced layouts (the random baseline of Section 4): for each layer in turn,
+    the contiguous h is shuffled, then the contiguous nu, drawing from one generator."""
+    hs, nus = [], []
+    c = 0
+    for _ in range(N):
+        h, c = _shuffle(contiguous_heads(G, L), seed, c)
+        nu, c = _shuffle(contiguous_neurons(I, L), seed, c)
+        hs.append(np.array(h, dtype=np.int64))
+        nus.append(np.array(nu, dtype=np.int64))
+    return hs, nus
+
+
+# ----------------------------------------------------------------------------- exact optimum
+def unlabelled_partitions(G: int, L: int) -> list:
+    """One labelled representative per balanced partition up to device relabelling: the
+    ones whose labels first appear in the order 0, 1, ..., L-1."""
+    out = []
+    for h in partitions(G, L):
+        firsts = [h.index(l) for l in range(L)]
+        if firsts == sorted(firsts):
+            out.append(h)
+    return out
+
+
+def layer_optimum(Q_up: np.ndarray, L: int):
+    """(h, nu, J_int) maximising one layer's co-located up mass exactly.
+
+    With no neighbours, relabelling devices maps optima to optima, so it suffices to take
+    every unlabelled head partition with its exact neuron assignment; the first partition
+    (lexicographic) that attains the maximum is returned with its canonical assignment.
+    """
+    G, _ = Q_up.shape
+    best = None
+    for h in unlabelled_partitions(G, L):
+        nu, val = balanced_assign(neuron_gain(Q_up, h, L))
+        if best is None or val > best[2]:
+            best = (tuple(h), nu, val)
+    return best

@@ -228,3 +228,65 @@ def test_silu_prime_is_derivative():
     torch.nn.functional.silu(gt).sum().backward()
     np.testing.assert_allclose(orc.silu_prime(g), gt.grad.numpy(), rtol=1e-13, atol=1e-15)
 
+
+
+# ----------------------------------------------------------------------------- ADD score
+def _preact_removal_add(d):
+    """sum_t (g(n) - g(n - p_h))^2 + (u(n) - u(n - p_h))^2 per head, via torch: [H, I]."""
+    x = torch.tensor(d["x"])
+    gam = torch.tensor(d["gamma"])
+    wg, wu = torch.tensor(d["w_gate"]), torch.tensor(d["w_up"])
+    wo = torch.tensor(d["w_o"])
+    attn = torch.tensor(d["attn"])
+    T, H, dh = attn.shape
+    r = torch.sqrt(torch.mean(x * x, dim=1, keepdim=True) + d["eps"])
+    n = gam * x / r
+    out = np.zeros((H, wg.shape[0]))
+    for h in range(H):
+        piece = gam * (attn[:, h, :] @ wo[:, h * dh:(h + 1) * dh].T) / r
+        dg = n @ wg.T - (n - piece) @ wg.T
+        du = n @ wu.T - (n - piece) @ wu.T
+        out[h] = (dg * dg + du * du).sum(0).numpy()
+    return out
+
+
+def test_add_equals_preactivation_removal(tiny):
+    per_head = _preact_removal_add(tiny)
+    H = per_head.shape[0]
+    G = tiny["n_kv_groups"]
+    ref = np.stack([per_head[[h for h in range(H) if h // (H // G) == g]].sum(0) for g in range(G)])
+    add = orc.affinity_add_literal(tiny["x"], tiny["attn"], tiny["w_o"], tiny["gamma"],
+                                   tiny["w_gate"], tiny["w_up"], G, tiny["eps"])
+    np.testing.assert_allclose(add, ref, rtol=1e-9)
+
+
+def test_add_folded_equals_literal(tiny):
+    kw = {k: v for k, v in tiny.items() if k != "w_down"}
+    np.testing.assert_allclose(orc.affinity_add_folded(**kw), orc.affinity_add_literal(**kw),
+                               rtol=1e-12)
+    sub = [0, 9, 127]
+    np.testing.assert_allclose(orc.affinity_add_folded(**kw, neurons=sub),
+                               orc.affinity_add_literal(**kw)[:, sub], rtol=1e-12)
+
+
+def test_add_ignores_operating_point_and_write(tiny):
+    """ADD depends on x only through r: the pre-activation levels and W_down do not enter."""
+    kw = {k: v for k, v in tiny.items() if k != "w_down"}
+    base = orc.affinity_add_literal(**kw)
+    # flip the sign of x: r is unchanged, g and u flip, ADD must not move
+    flipped = orc.affinity_add_literal(**dict(kw, x=-tiny["x"]))
+    np.testing.assert_allclose(flipped, base, rtol=1e-12)
+
+
+def test_add_head_scale_is_quadratic_and_local(tiny):
+    kw = {k: v for k, v in tiny.items() if k != "w_down"}
+    H = tiny["attn"].shape[1]
+    G = tiny["n_kv_groups"]
+    a = tiny["attn"].copy()
+    a[:, 5] *= 3.0
+    only = tiny["attn"] * 0.0
+    only[:, 5] = tiny["attn"][:, 5]
+    diff = orc.affinity_add_literal(**dict(kw, attn=a)) - orc.affinity_add_literal(**kw)
+    np.testing.assert_allclose(diff, 8.0 * orc.affinity_add_literal(**dict(kw, attn=only)),
+                               rtol=1e-10, atol=1e-14)
+    assert np.all(diff[np.arange(G) != 5 // (H // G)] == 0.0)

@@ -289,3 +289,72 @@ def test_random_expectation_matches_paper_table3(N, key):
     sem = np.std(Js) / np.sqrt(len(Js))
     assert abs(np.mean(Js) - float(exact)) < 5 * sem + 1e-9
     assert max(Js) <= 2 * N - 1
+
+
+# ----------------------------------------------------------------------------- random layouts
+def test_splitmix64_published_outputs():
+    path = os.path.join(os.path.dirname(__file__), "golden", "splitmix64.txt")
+    rows = [l.split() for l in open(path) if l.strip() and not l.startswith("#")]
+    for idx, val in rows:
+        assert lay.splitmix64(0, int(idx)) == int(val, 16)
+
+
+def test_random_layout_balanced_deterministic_and_seeded():
+    N, G, I, L = 3, 8, 64, 4
+    hs, nus = lay.random_layout(N, G, I, L, 1000)
+    for h, nu in zip(hs, nus):
+        assert sorted(np.bincount(h, minlength=L)) == [G // L] * L
+        assert sorted(np.bincount(nu, minlength=L)) == [I // L] * L
+    hs2, nus2 = lay.random_layout(N, G, I, L, 1000)
+    assert all(np.array_equal(a, b) for a, b in zip(hs + nus, hs2 + nus2))
+    hs3, _ = lay.random_layout(N, G, I, L, 1001)
+    assert any(not np.array_equal(a, b) for a, b in zip(hs, hs3))
+
+
+def test_random_layout_marginals_are_uniform():
+    """Each (group, device) pair occurs with frequency 1/L over seeds (chi-square)."""
+    G, I, L, S = 8, 8, 4, 4000
+    counts = np.zeros((G, L))
+    for seed in range(S):
+        hs, _ = lay.random_layout(1, G, I, L, seed)
+        counts[np.arange(G), hs[0]] += 1
+    expected = S / L
+    chi2 = ((counts - expected) ** 2 / expected).sum()
+    # G*(L-1) = 24 degrees of freedom (rows constrained); 99.99% quantile is about 56
+    assert chi2 < 60.0
+
+
+def test_random_layout_mean_J_is_edges_over_L():
+    gold = golden()
+    N, G, I, L = 28, 8, 64, 4
+    rng = np.random.default_rng(7)
+    Qu = [rand_Q(rng, (G, I)) for _ in range(N)]
+    Qd = [rand_Q(rng, (I, G)) for _ in range(N - 1)]
+    exact = Fraction(sum(int(q.sum()) for q in Qu + Qd), L) / 2 ** 48
+    Js = []
+    for seed in range(200):
+        hs, nus = lay.random_layout(N, G, I, L, seed)
+        Js.append(lay.objective(Qu, Qd, hs, nus) / 2 ** 48)
+    sem = np.std(Js) / np.sqrt(len(Js))
+    assert abs(np.mean(Js) - float(exact)) < 5 * sem + 1e-9
+    assert abs(float(exact) - gold["random_expectation_N28_L4"]) < 1e-9
+
+
+# ----------------------------------------------------------------------------- exact optimum
+@pytest.mark.parametrize("G,I,L,seed", [(4, 8, 2, 31), (6, 6, 3, 32), (4, 4, 4, 33)])
+def test_layer_optimum_equals_brute_force(G, I, L, seed):
+    rng = np.random.default_rng(seed)
+    hs_all, nus_all = all_layouts(G, I, L)
+    for _ in range(3):
+        Q = rand_Q(rng, (G, I))
+        h, nu, J = lay.layer_optimum(Q, L)
+        assert J == lay.objective([Q], None, [np.array(h)], [nu])
+        Jstar = max(lay.objective([Q], None, [hh], [n]) for hh in hs_all for n in nus_all)
+        assert J == Jstar
+        assert lay.coordinate_ascent([Q], None, L)[2] <= J
+
+
+def test_unlabelled_partition_counts():
+    for G, L in [(8, 4), (8, 2), (6, 3), (4, 2)]:
+        n = math.factorial(G) // (math.factorial(G // L) ** L * math.factorial(L))
+        assert len(lay.unlabelled_partitions(G, L)) == n

@@ -133,3 +133,42 @@ def test_down_value_rows_dropped_are_caught(tiny_down, monkeypatch):
     monkeypatch.setattr(dwn, "group_projection", bad)
     with pytest.raises(AssertionError):
         pd.test_equals_removal_through_next_projection(tiny_down)
+
+
+# ----------------------------------------------------------------------------- ADD, random, optimum
+def test_add_dropping_up_term_is_caught(tiny, monkeypatch):
+    def bad(x, attn, w_o, gamma, w_gate, w_up, n_kv_groups, eps, block=128):
+        T, H, _ = attn.shape
+        acc = np.zeros((H, w_gate.shape[0]))
+        p = orc.head_pieces(x, attn, w_o, gamma, eps)
+        acc += np.sum((p @ w_gate.T) ** 2, axis=0)
+        return orc._group_sum(acc, n_kv_groups)
+    monkeypatch.setattr(orc, "affinity_add_literal", bad)
+    with pytest.raises(AssertionError):
+        pa.test_add_equals_preactivation_removal(tiny)
+
+
+def test_sattolo_shuffle_is_caught(monkeypatch):
+    def bad(labels, seed, counter):  # i in [0, j): only cyclic permutations
+        a = list(labels)
+        for j in range(len(a) - 1, 0, -1):
+            r = lay.splitmix64(seed, counter)
+            counter += 1
+            i = (r * j) >> 64
+            a[j], a[i] = a[i], a[j]
+        return a, counter
+    monkeypatch.setattr(lay, "_shuffle", bad)
+    with pytest.raises(AssertionError):
+        pl.test_random_layout_marginals_are_uniform()
+
+
+def test_wrong_splitmix_constant_is_caught(monkeypatch):
+    monkeypatch.setattr(lay, "SPLITMIX_GAMMA", 0x9E3779B97F4A7C13)
+    with pytest.raises(AssertionError):
+        pl.test_splitmix64_published_outputs()
+
+
+def test_optimum_over_contiguous_heads_only_is_caught(monkeypatch):
+    monkeypatch.setattr(lay, "unlabelled_partitions", lambda G, L: [lay.contiguous_heads(G, L)])
+    with pytest.raises(AssertionError):
+        pl.test_layer_optimum_equals_brute_force(4, 8, 2, 31)
