@@ -97,6 +97,13 @@ dtp_status dtp_affinity_accumulate(dtp_layer layer, const void* x, const void* a
  *   x_next dev [n_tokens, d]  layer dtype, 16-byte aligned
  *   s_down dev [I] float       accumulated in place (+=); deterministic for fixed shapes
  * x_next and s_down are both required (DTP_ERR_INVALID_ARG otherwise). */
+/* The simpler ADD score of Section 3 ("Affinity scores") over the same token stream:
+ *   A[g, k] += sum_t sum_{h in g} (p_h . w^g_k)^2 + (p_h . w^u_k)^2,
+ * which ignores the operating point of the nonlinearity and the neuron's write (no
+ * ||w^d_k||^2 factor).  Arguments as for dtp_affinity_accumulate. */
+dtp_status dtp_affinity_accumulate_add(dtp_layer layer, const void* x, const void* attn,
+                                       int64_t n_tokens, float* A, void* stream);
+
 dtp_status dtp_affinity_accumulate_down(dtp_layer layer, const void* x, const void* attn,
                                         const void* x_next, float rms_eps_next,
                                         int64_t n_tokens, float* A, float* s_down,
@@ -215,6 +222,32 @@ dtp_status dtp_coordinate_ascent(int32_t N, int32_t G, int32_t I, int32_t L,
                                  const float* A_up, const float* A_down,
                                  const dtp_ca_options* options, int32_t* h, int32_t* nu,
                                  int64_t* J_fixed, double* J, int32_t* sweeps, void* stream);
+
+/* Seeded balanced layouts, the random baseline of the ablations (Section 4): for each
+ * layer in turn, the contiguous h_i (h(g) = g/(G/L)) and then the contiguous nu_i are
+ * shuffled by Fisher-Yates from the last position down, position j swapping with
+ * floor(r (j+1) / 2^64), r the next output of SplitMix64 (Steele, Lea and Flood, 2014)
+ * started from state `seed`.  h host [N, G] and nu host [N, I] int32 outputs.  Host only. */
+dtp_status dtp_random_layout(int32_t N, int32_t G, int32_t I, int32_t L, uint64_t seed,
+                             int32_t* h, int32_t* nu);
+
+/* J_int of a given layout (Section 3, eq. "objective"): the sum of co-located codes over
+ * the N up edges and, when Q_down is given, the N-1 down edges.
+ *   Q_up host [N, G, I] and Q_down host [N-1, I, G] or NULL: dtp_encode_affinity codes
+ *   h host [N, G], nu host [N, I]: balanced layouts (DTP_ERR_INVALID_ARG otherwise)
+ *   J_fixed host int64 output; J = J_fixed / 2^48.  Host only. */
+dtp_status dtp_layout_objective(int32_t N, int32_t G, int32_t I, int32_t L, const int64_t* Q_up,
+                                const int64_t* Q_down, const int32_t* h, const int32_t* nu,
+                                int64_t* J_fixed);
+
+/* Exact optimum of one layer's up edge: every head partition up to device relabelling
+ * (labels first appearing in the order 0..L-1; 105 at G=8, L=4) with its exact neuron
+ * assignment; the first such partition in lexicographic order that attains the maximum
+ * is returned with its canonical assignment.  Bounds the coordinate ascent from above.
+ *   Q_up host [G, I] codes; h host [G], nu host [I] outputs; J_fixed host output.
+ * Host only (one thread per partition, at most 16). */
+dtp_status dtp_layer_optimum(int32_t G, int32_t I, int32_t L, const int64_t* Q_up, int32_t* h,
+                             int32_t* nu, int64_t* J_fixed);
 
 /* Human-readable name of a status code (static storage). */
 const char* dtp_status_string(dtp_status status);

@@ -2,6 +2,7 @@
 // the encoder, partition enumeration, the neuron step and the coordinate-ascent driver
 // (Section 3, "Objective" and "Optimiser").  The affinity entry points live in
 // affinity.hip.
+#include <algorithm>
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
@@ -93,6 +94,23 @@ int64_t objective_int(int N, int G, int I, const std::vector<int64_t>& Qu,
     }
   }
   return J;
+}
+
+// SplitMix64 output n from state `seed` (Steele, Lea and Flood, OOPSLA 2014).
+uint64_t splitmix64(uint64_t seed, uint64_t n) {
+  uint64_t z = seed + (n + 1) * 0x9E3779B97F4A7C15ull;
+  z = (z ^ (z >> 30)) * 0xBF58476D1CE4E5B9ull;
+  z = (z ^ (z >> 27)) * 0x94D049BB133111EBull;
+  return z ^ (z >> 31);
+}
+
+// Fisher-Yates from the last position down; position j swaps with floor(r (j+1) / 2^64).
+void shuffle(int32_t* a, int n, uint64_t seed, uint64_t* counter) {
+  for (int j = n - 1; j > 0; --j) {
+    const uint64_t r = splitmix64(seed, (*counter)++);
+    const int i = (int)(((unsigned __int128)r * (uint64_t)(j + 1)) >> 64);
+    std::swap(a[j], a[i]);
+  }
 }
 
 struct DevBuf {
@@ -342,6 +360,101 @@ dtp_status dtp_coordinate_ascent(int32_t N, int32_t G, int32_t I, int32_t L, con
   *J_fixed = J_prev;
   *J = (double)J_prev / (double)(int64_t(1) << kFracBits);
   *sweeps = sweep;
+  return DTP_OK;
+}
+
+dtp_status dtp_random_layout(int32_t N, int32_t G, int32_t I, int32_t L, uint64_t seed,
+                             int32_t* h, int32_t* nu) {
+  clear_error();
+  DTP_CHECK(N >= 1, DTP_ERR_INVALID_ARG, "N=%d must be >= 1", N);
+  dtp_status st = check_layout_sizes(G, I, L, kMaxGroups);
+  if (st != DTP_OK) return st;
+  DTP_CHECK(h && nu, DTP_ERR_INVALID_ARG, "h or nu is NULL");
+  uint64_t counter = 0;
+  for (int i = 0; i < N; ++i) {
+    int32_t* hi = h + (size_t)i * G;
+    int32_t* ni = nu + (size_t)i * I;
+    for (int g = 0; g < G; ++g) hi[g] = g / (G / L);
+    shuffle(hi, G, seed, &counter);
+    for (int k = 0; k < I; ++k) ni[k] = k / (I / L);
+    shuffle(ni, I, seed, &counter);
+  }
+  return DTP_OK;
+}
+
+dtp_status dtp_layout_objective(int32_t N, int32_t G, int32_t I, int32_t L, const int64_t* Q_up,
+                                const int64_t* Q_down, const int32_t* h, const int32_t* nu,
+                                int64_t* J_fixed) {
+  clear_error();
+  DTP_CHECK(N >= 1, DTP_ERR_INVALID_ARG, "N=%d must be >= 1", N);
+  dtp_status st = check_layout_sizes(G, I, L, kMaxGroups);
+  if (st != DTP_OK) return st;
+  DTP_CHECK(Q_up && h && nu && J_fixed, DTP_ERR_INVALID_ARG, "a required pointer is NULL");
+  DTP_CHECK(Q_down == nullptr || N >= 2, DTP_ERR_INVALID_ARG, "Q_down needs N >= 2");
+  for (int i = 0; i < N; ++i) {
+    if ((st = check_balanced(h + (size_t)i * G, G, L, "h")) != DTP_OK) return st;
+    std::vector<int32_t> cnt(L, 0);
+    for (int k = 0; k < I; ++k) {
+      const int32_t l = nu[(size_t)i * I + k];
+      DTP_CHECK(l >= 0 && l < L, DTP_ERR_INVALID_ARG, "nu[%d][%d] = %d is not a device", i, k, l);
+      ++cnt[l];
+    }
+    for (int l = 0; l < L; ++l)
+      DTP_CHECK(cnt[l] == I / L, DTP_ERR_INVALID_ARG, "nu[%d] is not balanced", i);
+  }
+  const size_t nup = (size_t)N * G * I, ndown = Q_down ? (size_t)(N - 1) * I * G : 0;
+  std::vector<int64_t> Qu(Q_up, Q_up + nup), Qd;
+  if (Q_down) Qd.assign(Q_down, Q_down + ndown);
+  std::vector<int32_t> hv(h, h + (size_t)N * G), nv(nu, nu + (size_t)N * I);
+  *J_fixed = objective_int(N, G, I, Qu, Qd, Q_down != nullptr, hv, nv);
+  return DTP_OK;
+}
+
+dtp_status dtp_layer_optimum(int32_t G, int32_t I, int32_t L, const int64_t* Q_up, int32_t* h,
+                             int32_t* nu, int64_t* J_fixed) {
+  clear_error();
+  dtp_status st = check_layout_sizes(G, I, L, kMaxAssignDevices);
+  if (st != DTP_OK) return st;
+  DTP_CHECK(Q_up && h && nu && J_fixed, DTP_ERR_INVALID_ARG, "a required pointer is NULL");
+  const int64_t P = count_partitions(G, L);
+  DTP_CHECK(P > 0 && P <= kMaxPartitions, DTP_ERR_UNSUPPORTED, "too many partitions (%lld)",
+            (long long)P);
+  // One representative per partition up to device relabelling: labels first appear in
+  // the order 0, 1, ..., L-1.
+  const std::vector<uint8_t> table = enumerate_partitions(G, L);
+  std::vector<int64_t> reps;
+  for (int64_t r = 0; r < P; ++r) {
+    const uint8_t* hp = table.data() + (size_t)r * G;
+    int next = 0;
+    bool ok = true;
+    for (int g = 0; g < G && ok; ++g) {
+      if (hp[g] > next) ok = false;
+      else if (hp[g] == next) ++next;
+    }
+    if (ok) reps.push_back(r);
+  }
+  std::vector<int64_t> value(reps.size());
+  std::vector<std::vector<int32_t>> nus(reps.size(), std::vector<int32_t>(I));
+  auto solve = [&](size_t j) {
+    int32_t hh[kMaxGroups];
+    for (int g = 0; g < G; ++g) hh[g] = table[(size_t)reps[j] * G + g];
+    std::vector<int64_t> M;
+    neuron_gain(G, I, L, Q_up, hh, nullptr, nullptr, false, &M);
+    balanced_assign_exact(I, L, M.data(), nus[j].data(), &value[j]);
+  };
+  const unsigned hw = std::max(1u, std::min(16u, std::thread::hardware_concurrency()));
+  std::vector<std::thread> pool;
+  for (unsigned t = 0; t < hw; ++t)
+    pool.emplace_back([&, t] {
+      for (size_t j = t; j < reps.size(); j += hw) solve(j);
+    });
+  for (auto& th : pool) th.join();
+  size_t best = 0;  // first partition (lexicographic) attaining the maximum
+  for (size_t j = 1; j < reps.size(); ++j)
+    if (value[j] > value[best]) best = j;
+  for (int g = 0; g < G; ++g) h[g] = table[(size_t)reps[best] * G + g];
+  std::copy(nus[best].begin(), nus[best].end(), nu);
+  *J_fixed = value[best];
   return DTP_OK;
 }
 

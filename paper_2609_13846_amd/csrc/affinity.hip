@@ -452,7 +452,7 @@ __device__ __forceinline__ void block_work(int b, int n_tg, int n_split, int& tg
 // are kept per lane over its rows, folded across the two half-waves after the last query
 // head of each KV group, and banked in LDS per (wave, group); the block writes the
 // fixed-order sum over its WM row waves times ||w^d_k||^2 to its split's partial.
-template <int KC, int WM, int WN, int RB, int NB, bool PACK, int SG>
+template <int KC, int WM, int WN, int RB, int NB, bool PACK, int SG, bool ADD>
 __global__ void __launch_bounds__(64 * WM * WN, 2)  // two waves per SIMD
 affinity_bf16_kernel(AffinityArgs p) {
   constexpr int NT = 64 * WM * WN;
@@ -562,7 +562,10 @@ affinity_bf16_kernel(AffinityArgs p) {
                 const float g = acc[rb][nb][0][i] * ri;
                 const float u = acc[rb][nb][1][i] * ri;
                 const float sg = __builtin_amdgcn_rcpf(1.0f + __expf(-g));
-                cf.set(rb, nb, i, sg * (1.0f + g * (1.0f - sg)) * u * rs, g * sg * rs);
+                if (ADD)
+                  cf.set(rb, nb, i, rs, rs);
+                else
+                  cf.set(rb, nb, i, sg * (1.0f + g * (1.0f - sg)) * u * rs, g * sg * rs);
               }
             }
           }
@@ -602,8 +605,14 @@ affinity_bf16_kernel(AffinityArgs p) {
           for (int nb = 0; nb < NB; ++nb)
 #pragma unroll
             for (int i = 0; i < 16; ++i) {
-              const float dl = cf.c1(rb, nb, i) * acc[rb][nb][0][i] + cf.c2(rb, nb, i) * acc[rb][nb][1][i];
-              colsum[nb] = fmaf(dl, dl, colsum[nb]);
+              if (ADD) {  // (p_h . w^g_k)^2 + (p_h . w^u_k)^2, both coefficients 1/r
+                const float dg = cf.c1(rb, nb, i) * acc[rb][nb][0][i];
+                const float du = cf.c2(rb, nb, i) * acc[rb][nb][1][i];
+                colsum[nb] = fmaf(du, du, fmaf(dg, dg, colsum[nb]));
+              } else {
+                const float dl = cf.c1(rb, nb, i) * acc[rb][nb][0][i] + cf.c2(rb, nb, i) * acc[rb][nb][1][i];
+                colsum[nb] = fmaf(dl, dl, colsum[nb]);
+              }
             }
         head_stage = 0;
         if (h % hpg == hpg - 1) {
@@ -645,12 +654,12 @@ affinity_bf16_kernel(AffinityArgs p) {
     float sum = 0.0f;
     for (int w = 0; w < WM; ++w) sum += red[((cw * WM + w) * G1 + g) * (32 * NB) + k];
     const int n = tg * kNeurons + nl;
-    p.partial[((int64_t)split * G1 + g) * p.I_pad + n] = g < p.G ? sum * p.nd[n] : sum;
+    p.partial[((int64_t)split * G1 + g) * p.I_pad + n] = g < p.G && !ADD ? sum * p.nd[n] : sum;
   }
 }
 
 // Launches the fused kernel on one slice; returns the number of token splits used.
-template <int KC, int WM, int WN, int RB, int NB, bool PACK = false, int SG = 4>
+template <int KC, int WM, int WN, int RB, int NB, bool PACK = false, int SG = 4, bool ADD = false>
 int launch_affinity(AffinityArgs p, hipStream_t s) {
   constexpr int kRows = 32 * RB * WM;
   constexpr int kNeurons = 32 * NB * WN;
@@ -659,9 +668,9 @@ int launch_affinity(AffinityArgs p, hipStream_t s) {
   p.splits = std::max(1, std::min((kTargetBlocks + groups - 1) / groups, std::min(mtiles, kMaxSplits)));
   const size_t shm = sizeof(float) * WM * WN * (p.G + 1) * 32 * NB;
   if (shm > 65536)  // beyond the default dynamic LDS limit (G close to 32)
-    (void)hipFuncSetAttribute((const void*)&affinity_bf16_kernel<KC, WM, WN, RB, NB, PACK, SG>,
+    (void)hipFuncSetAttribute((const void*)&affinity_bf16_kernel<KC, WM, WN, RB, NB, PACK, SG, ADD>,
                               hipFuncAttributeMaxDynamicSharedMemorySize, (int)shm);
-  affinity_bf16_kernel<KC, WM, WN, RB, NB, PACK, SG><<<groups * p.splits, 64 * WM * WN, shm, s>>>(p);
+  affinity_bf16_kernel<KC, WM, WN, RB, NB, PACK, SG, ADD><<<groups * p.splits, 64 * WM * WN, shm, s>>>(p);
   return p.splits;
 }
 
@@ -677,6 +686,7 @@ struct AffinityF32Args {
   const float* nd;
   float* partial;      // [splits][G+1][I_pad]
   int T, d, H, G, dh, I, I_pad, splits;
+  int add;             // ADD score instead of FO
 };
 
 __global__ void __launch_bounds__(256)
@@ -709,8 +719,8 @@ affinity_f32_kernel(AffinityF32Args p) {
         const float a = g * sg * u * p.rinv_next[t];
         acc[p.G] = fmaf(a, a, acc[p.G]);
       }
-      const float cc2 = g * sg * ri;
-      const float cc1 = sg * (1.0f + g * (1.0f - sg)) * u * ri;
+      const float cc2 = p.add ? ri : g * sg * ri;
+      const float cc1 = p.add ? ri : sg * (1.0f + g * (1.0f - sg)) * u * ri;
       for (int h = 0; h < p.H; ++h) {
         const float* ar = p.attn + (int64_t)t * HD + h * p.dh;
         const float* fg = p.fold + (((int64_t)h * 2 + 0) * p.I + k) * p.dh;
@@ -720,8 +730,12 @@ affinity_f32_kernel(AffinityF32Args p) {
           pg = fmaf(ar[e], fg[e], pg);
           pu = fmaf(ar[e], fu[e], pu);
         }
-        const float dl = cc1 * pg + cc2 * pu;
-        acc[h / hpg] = fmaf(dl, dl, acc[h / hpg]);
+        if (p.add) {
+          acc[h / hpg] = fmaf(cc1 * pg, cc1 * pg, fmaf(cc2 * pu, cc2 * pu, acc[h / hpg]));
+        } else {
+          const float dl = cc1 * pg + cc2 * pu;
+          acc[h / hpg] = fmaf(dl, dl, acc[h / hpg]);
+        }
       }
     }
   }
@@ -731,7 +745,7 @@ affinity_f32_kernel(AffinityF32Args p) {
     const int g = i / kBN, kk = i % kBN;
     const float s = red[0][g][kk] + red[1][g][kk] + red[2][g][kk] + red[3][g][kk];
     const int n = tile * kBN + kk;
-    p.partial[((int64_t)split * (p.G + 1) + g) * p.I_pad + n] = g < p.G ? s * p.nd[n] : s;
+    p.partial[((int64_t)split * (p.G + 1) + g) * p.I_pad + n] = g < p.G && !p.add ? s * p.nd[n] : s;
   }
 }
 
@@ -809,7 +823,8 @@ namespace {
 // Shared body of the two accumulate entry points; x_next / s_down are NULL for the up
 // affinity alone.
 dtp_status accumulate(dtp_layer L, const void* x, const void* attn, const void* x_next,
-                      float eps_next, int64_t n_tokens, float* A, float* s_down, void* stream) {
+                      float eps_next, int64_t n_tokens, float* A, float* s_down, bool add,
+                      void* stream) {
   DTP_CHECK(L != nullptr, DTP_ERR_INVALID_ARG, "layer is NULL");
   DTP_CHECK(n_tokens >= 0, DTP_ERR_INVALID_ARG, "n_tokens=%lld is negative", (long long)n_tokens);
   if (n_tokens == 0) return DTP_OK;
@@ -898,11 +913,14 @@ dtp_status accumulate(dtp_layer L, const void* x, const void* attn, const void* 
       // Eight wavefronts per block (one block per CU): 256 tokens x 64 neurons per tile;
       // four for 16-wide stages, whose weight stage has only 256 16-byte pieces.
       if (kc == 64)
-        splits = launch_affinity<64, 8, 1, 1, 2, true>(p, s);
+        splits = add ? launch_affinity<64, 8, 1, 1, 2, true, 4, true>(p, s)
+                     : launch_affinity<64, 8, 1, 1, 2, true, 4, false>(p, s);
       else if (kc == 32)
-        splits = launch_affinity<32, 8, 1, 1, 2, true>(p, s);
+        splits = add ? launch_affinity<32, 8, 1, 1, 2, true, 4, true>(p, s)
+                     : launch_affinity<32, 8, 1, 1, 2, true, 4, false>(p, s);
       else
-        splits = launch_affinity<16, 4, 1, 1, 2, true>(p, s);
+        splits = add ? launch_affinity<16, 4, 1, 1, 2, true, 4, true>(p, s)
+                     : launch_affinity<16, 4, 1, 1, 2, true, 4, false>(p, s);
     } else {
       splits = (kTargetBlocks / 4 + L->n_tiles - 1) / L->n_tiles;
       splits = std::max(1, std::min(splits, std::min(T, kMaxSplits)));
@@ -923,6 +941,7 @@ dtp_status accumulate(dtp_layer L, const void* x, const void* attn, const void* 
       p.I = I;
       p.I_pad = L->I_pad;
       p.splits = splits;
+      p.add = add ? 1 : 0;
       affinity_f32_kernel<<<L->n_tiles * splits, 256, 0, s>>>(p);
     }
     DTP_HIP(hipGetLastError());
@@ -1053,7 +1072,13 @@ dtp_status dtp_layer_set_weights(dtp_layer L, const void* w_o, const void* gamma
 dtp_status dtp_affinity_accumulate(dtp_layer L, const void* x, const void* attn, int64_t n_tokens,
                                    float* A, void* stream) {
   clear_error();
-  return dtp::accumulate(L, x, attn, nullptr, 0.0f, n_tokens, A, nullptr, stream);
+  return dtp::accumulate(L, x, attn, nullptr, 0.0f, n_tokens, A, nullptr, false, stream);
+}
+
+dtp_status dtp_affinity_accumulate_add(dtp_layer L, const void* x, const void* attn,
+                                       int64_t n_tokens, float* A, void* stream) {
+  clear_error();
+  return dtp::accumulate(L, x, attn, nullptr, 0.0f, n_tokens, A, nullptr, true, stream);
 }
 
 dtp_status dtp_affinity_accumulate_down(dtp_layer L, const void* x, const void* attn,
@@ -1061,7 +1086,7 @@ dtp_status dtp_affinity_accumulate_down(dtp_layer L, const void* x, const void* 
                                         float* A, float* s_down, void* stream) {
   clear_error();
   DTP_CHECK(x_next && s_down, DTP_ERR_INVALID_ARG, "x_next or s_down is NULL");
-  return dtp::accumulate(L, x, attn, x_next, rms_eps_next, n_tokens, A, s_down, stream);
+  return dtp::accumulate(L, x, attn, x_next, rms_eps_next, n_tokens, A, s_down, false, stream);
 }
 
 dtp_status dtp_layer_profile(dtp_layer L, int32_t enable) {

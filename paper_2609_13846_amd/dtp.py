@@ -51,6 +51,10 @@ _SIGNATURES = {
     "dtp_layer_destroy": (_I32, [_P]),
     "dtp_layer_set_weights": (_I32, [_P, _P, _P, _P, _P, _P, _P]),
     "dtp_affinity_accumulate": (_I32, [_P, _P, _P, _I64, _P, _P]),
+    "dtp_affinity_accumulate_add": (_I32, [_P, _P, _P, _I64, _P, _P]),
+    "dtp_random_layout": (_I32, [_I32, _I32, _I32, _I32, ctypes.c_uint64, _P, _P]),
+    "dtp_layout_objective": (_I32, [_I32, _I32, _I32, _I32, _P, _P, _P, _P, ctypes.POINTER(_I64)]),
+    "dtp_layer_optimum": (_I32, [_I32, _I32, _I32, _P, _P, _P, ctypes.POINTER(_I64)]),
     "dtp_affinity_accumulate_down": (_I32, [_P, _P, _P, _P, ctypes.c_float, _I64, _P, _P, _P]),
     "dtp_down_weights": (_I32, [_I32, _I32, _I32, _I32, _I32, _I32, _P, _P, _P, _P, _P, _P, _P]),
     "dtp_down_affinity": (_I32, [_I32, _I32, _P, _P, _P, _P]),
@@ -148,6 +152,11 @@ def dtp_affinity_accumulate(layer, x, attn, n_tokens, A, stream=None):
                                          _stream(stream)))
 
 
+def dtp_affinity_accumulate_add(layer, x, attn, n_tokens, A, stream=None):
+    _check(lib().dtp_affinity_accumulate_add(layer, _ptr(x), _ptr(attn), int(n_tokens), _ptr(A),
+                                             _stream(stream)))
+
+
 def dtp_affinity_accumulate_down(layer, x, attn, x_next, rms_eps_next, n_tokens, A, s_down,
                                  stream=None):
     _check(lib().dtp_affinity_accumulate_down(layer, _ptr(x), _ptr(attn), _ptr(x_next),
@@ -234,3 +243,33 @@ def dtp_coordinate_ascent(N, G, I, L, A_up, A_down=None, max_sweeps=64, freeze_h
                                        _ptr(h), _ptr(nu), ctypes.byref(jf), ctypes.byref(j),
                                        ctypes.byref(sw), _stream(stream)))
     return {"h": h, "nu": nu, "J_fixed": jf.value, "J": j.value, "sweeps": sw.value}
+
+
+def dtp_random_layout(N, G, I, L, seed):
+    """(h [N, G], nu [N, I]) int32 host arrays of the seeded balanced layouts."""
+    h = np.zeros((N, G), dtype=np.int32)
+    nu = np.zeros((N, I), dtype=np.int32)
+    _check(lib().dtp_random_layout(N, G, I, L, ctypes.c_uint64(seed & (2 ** 64 - 1)), _ptr(h), _ptr(nu)))
+    return h, nu
+
+
+def dtp_layout_objective(N, G, I, L, Q_up, Q_down, h, nu):
+    """J_int of a layout from host codes (int64 arrays), as a Python int."""
+    Q_up = np.ascontiguousarray(Q_up, dtype=np.int64)
+    Q_down = None if Q_down is None else np.ascontiguousarray(Q_down, dtype=np.int64)
+    h = np.ascontiguousarray(h, dtype=np.int32)
+    nu = np.ascontiguousarray(nu, dtype=np.int32)
+    J = _I64()
+    _check(lib().dtp_layout_objective(N, G, I, L, _ptr(Q_up), _ptr(Q_down), _ptr(h), _ptr(nu),
+                                      ctypes.byref(J)))
+    return int(J.value)
+
+
+def dtp_layer_optimum(G, I, L, Q_up):
+    """(h [G], nu [I], J_int) of one layer's exact optimum from host codes."""
+    Q_up = np.ascontiguousarray(Q_up, dtype=np.int64)
+    h = np.zeros(G, dtype=np.int32)
+    nu = np.zeros(I, dtype=np.int32)
+    J = _I64()
+    _check(lib().dtp_layer_optimum(G, I, L, _ptr(Q_up), _ptr(h), _ptr(nu), ctypes.byref(J)))
+    return h, nu, int(J.value)

@@ -24,8 +24,9 @@ def layer_for(wl: synth.Workload):
 
 
 def gpu_affinity(wl: synth.Workload, w: synth.LayerWeights, x: np.ndarray, a: np.ndarray,
-                 chunks=None, A0=None) -> np.ndarray:
-    """A [G, I] float32 from the library, accumulated over token chunks (sizes)."""
+                 chunks=None, A0=None, score="fo") -> np.ndarray:
+    """A [G, I] float32 from the library, accumulated over token chunks (sizes); score
+    "fo" (first order) or "add"."""
     import torch
     T = x.shape[0]
     layer = layer_for(wl)
@@ -41,7 +42,8 @@ def gpu_affinity(wl: synth.Workload, w: synth.LayerWeights, x: np.ndarray, a: np
             bounds.append(bounds[-1] + c)
         assert bounds[-1] == T
         for t0, t1 in zip(bounds, bounds[1:]):
-            dtp.dtp_affinity_accumulate(layer, dx[t0:t1], da[t0:t1], t1 - t0, A)
+            fn = dtp.dtp_affinity_accumulate if score == "fo" else dtp.dtp_affinity_accumulate_add
+            fn(layer, dx[t0:t1], da[t0:t1], t1 - t0, A)
         torch.cuda.synchronize()
         return A.cpu().numpy()
     finally:

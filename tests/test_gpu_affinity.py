@@ -126,3 +126,46 @@ def test_neuron_permutation_equivariance():
     A2 = hp.gpu_affinity(wl, w2, x, a)
     # each (group, neuron) entry is computed independently of its tile position
     np.testing.assert_array_equal(A2, A[:, perm])
+
+
+# ----------------------------------------------------------------------------- ADD score
+def add_oracle(wl, w, x, a, neurons=None):
+    kw = hp.oracle_inputs(w, x, a)
+    kw.pop("w_down")
+    return orc.affinity_add_folded(**kw, n_kv_groups=wl.n_kv_groups, eps=wl.rms_eps, neurons=neurons)
+
+
+@pytest.mark.parametrize("name,T,shape", [
+    ("tiny", 512, {}),
+    ("qwen3-0.6b-layer", 300, {}),
+    ("danube3-500m", 257, {}),
+    ("danube3-500m", 64, dict(d_model=272, n_neurons=192)),         # 16-deep stages
+    ("qwen3-0.6b-layer", 100, dict(n_q_heads=32, n_kv_groups=32, head_dim=64)),
+])
+def test_add_score_matches_oracle(name, T, shape):
+    wl, w, x, a = case(name, T, **shape)
+    announce(f"add score {name} T={T} {shape}")
+    A = hp.gpu_affinity(wl, w, x, a, score="add")
+    hp.assert_affinity_close(A, add_oracle(wl, w, x, a))
+
+
+def test_add_score_full_qwen_layer_sampled_neurons():
+    wl, w, x, a = case("qwen3-0.6b-layer", 65536)
+    announce("add score qwen 65536 sampled neurons")
+    A = hp.gpu_affinity(wl, w, x, a, score="add")
+    cols = np.r_[0:32, 1500:1532, wl.n_neurons - 32:wl.n_neurons]
+    hp.assert_affinity_close(A[:, cols], add_oracle(wl, w, x, a, neurons=cols))
+
+
+def test_add_score_power_of_two_head_scale_is_exact():
+    wl, w, x, a = case("qwen3-0.6b-layer", 300)
+    H, G = wl.n_q_heads, wl.n_kv_groups
+    g = 3
+    heads = [h for h in range(H) if h // (H // G) == g]
+    a2 = synth.to_f64(a).copy()
+    a2[:, heads] *= 2.0
+    a2 = synth.store(a2, "bf16")
+    A1 = hp.gpu_affinity(wl, w, x, a, score="add")
+    A2 = hp.gpu_affinity(wl, w, x, a2, score="add")
+    np.testing.assert_array_equal(A2[g], 4.0 * A1[g])
+    np.testing.assert_array_equal(np.delete(A2, g, axis=0), np.delete(A1, g, axis=0))

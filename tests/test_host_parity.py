@@ -79,3 +79,45 @@ def test_balanced_assign_ties_bit_exact(I, L):
     Z = np.zeros((G, I), np.int64)
     nu, v = dtp.dtp_balanced_assign(G, I, L, Z, np.arange(G) // (G // L))
     np.testing.assert_array_equal(nu, np.arange(I) // (I // L))
+
+
+# ----------------------------------------------------------------------------- random layouts
+@pytest.mark.parametrize("N,G,I,L,seed", [(1, 8, 64, 4, 1000), (3, 8, 3072, 2, 1007),
+                                           (2, 4, 128, 2, 0), (2, 16, 96, 8, 2 ** 64 - 1)])
+def test_random_layout_bit_exact(N, G, I, L, seed):
+    h, nu = dtp.dtp_random_layout(N, G, I, L, seed)
+    hs, nus = lay.random_layout(N, G, I, L, seed)
+    np.testing.assert_array_equal(h, np.array(hs))
+    np.testing.assert_array_equal(nu, np.array(nus))
+
+
+# ----------------------------------------------------------------------------- objective
+@pytest.mark.parametrize("down", [False, True])
+def test_layout_objective_bit_exact(down):
+    rng = np.random.default_rng(41)
+    N, G, I, L = 3, 8, 256, 4
+    Qu = [lay.encode(rand_A(rng, (G, I))) for _ in range(N)]
+    Qd = [lay.encode(rand_A(rng, (I, G))) for _ in range(N - 1)] if down else None
+    hs, nus = lay.random_layout(N, G, I, L, 5)
+    J = dtp.dtp_layout_objective(N, G, I, L, np.stack(Qu), None if Qd is None else np.stack(Qd),
+                                 np.array(hs), np.array(nus))
+    assert J == lay.objective(Qu, Qd, hs, nus)
+
+
+def test_layout_objective_rejects_unbalanced():
+    G, I, L = 4, 8, 2
+    Q = lay.encode(rand_A(np.random.default_rng(0), (G, I)))
+    with pytest.raises(dtp.DtpError):
+        dtp.dtp_layout_objective(1, G, I, L, Q, None, np.array([[0, 0, 0, 1]]), np.zeros((1, I)))
+
+
+# ----------------------------------------------------------------------------- exact optimum
+@pytest.mark.parametrize("G,I,L,seed", [(8, 64, 4, 51), (8, 128, 2, 52), (4, 16, 2, 53), (6, 24, 3, 54)])
+def test_layer_optimum_bit_exact(G, I, L, seed):
+    rng = np.random.default_rng(seed)
+    Q = lay.encode(rand_A(rng, (G, I)))
+    h, nu, J = dtp.dtp_layer_optimum(G, I, L, Q)
+    rh, rnu, rJ = lay.layer_optimum(Q, L)
+    assert J == rJ
+    np.testing.assert_array_equal(h, np.array(rh))
+    np.testing.assert_array_equal(nu, rnu)
