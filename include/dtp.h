@@ -249,6 +249,31 @@ dtp_status dtp_layout_objective(int32_t N, int32_t G, int32_t I, int32_t L, cons
 dtp_status dtp_layer_optimum(int32_t G, int32_t I, int32_t L, const int64_t* Q_up, int32_t* h,
                              int32_t* nu, int64_t* J_fixed);
 
+/* ---------------------------------------------------------------------------------------
+ * Applying a layout (Section 3, "Problem").  Device l's shard holds the KV groups and
+ * neurons that (h, nu) put on l, in increasing original index; shards follow in device
+ * order.  The permuted layer computes the same function (rotary embeddings, per-head norms
+ * and SwiGLU act per head or per neuron).
+ * ------------------------------------------------------------------------------------- */
+
+/* New position -> original index of the groups ([G]) and neurons ([I]).  Host only;
+ * DTP_ERR_INVALID_ARG unless h and nu are balanced assignments to L devices. */
+dtp_status dtp_layout_orders(int32_t G, int32_t I, int32_t L, const int32_t* h, const int32_t* nu,
+                             int32_t* group_order, int32_t* neuron_order);
+
+/* Permuted copies of one decoder layer's weights.  src and dst hold 7 device pointers,
+ * in the order w_q [H*dh, d], w_k [G*dh, d], w_v [G*dh, d], w_o [d, H*dh],
+ * w_gate [I, d], w_up [I, d], w_down [d, I] (PyTorch weight layouts, desc->dtype,
+ * 16-byte aligned, d * element size a multiple of 16 bytes).  Rows of w_q (by query-head
+ * blocks of a group), w_k, w_v and columns of w_o move with the groups; rows of w_gate,
+ * w_up and columns of w_down move with the neurons.  Gains and per-head norm weights are
+ * unchanged and not touched.  h host [G], nu host [I].  dst must not alias src.
+ * Bit-exact data movement; a [G + I] int32 scratch comes from the stream-ordered
+ * allocator and is returned before exit. */
+dtp_status dtp_apply_layout(const dtp_layer_desc* desc, int32_t L, const int32_t* h,
+                            const int32_t* nu, const void* const* src, void* const* dst,
+                            void* stream);
+
 /* Human-readable name of a status code (static storage). */
 const char* dtp_status_string(dtp_status status);
 

@@ -51,6 +51,8 @@ _SIGNATURES = {
     "dtp_layer_destroy": (_I32, [_P]),
     "dtp_layer_set_weights": (_I32, [_P, _P, _P, _P, _P, _P, _P]),
     "dtp_affinity_accumulate": (_I32, [_P, _P, _P, _I64, _P, _P]),
+    "dtp_layout_orders": (_I32, [_I32, _I32, _I32, _P, _P, _P, _P]),
+    "dtp_apply_layout": (_I32, [ctypes.POINTER(dtp_layer_desc), _I32, _P, _P, _P, _P, _P]),
     "dtp_affinity_accumulate_add": (_I32, [_P, _P, _P, _I64, _P, _P]),
     "dtp_random_layout": (_I32, [_I32, _I32, _I32, _I32, ctypes.c_uint64, _P, _P]),
     "dtp_layout_objective": (_I32, [_I32, _I32, _I32, _I32, _P, _P, _P, _P, ctypes.POINTER(_I64)]),
@@ -273,3 +275,29 @@ def dtp_layer_optimum(G, I, L, Q_up):
     J = _I64()
     _check(lib().dtp_layer_optimum(G, I, L, _ptr(Q_up), _ptr(h), _ptr(nu), ctypes.byref(J)))
     return h, nu, int(J.value)
+
+
+def dtp_layout_orders(G, I, L, h, nu):
+    """(group_order [G], neuron_order [I]) int32: new position -> original index."""
+    h = np.ascontiguousarray(h, dtype=np.int32)
+    nu = np.ascontiguousarray(nu, dtype=np.int32)
+    go = np.zeros(G, dtype=np.int32)
+    no = np.zeros(I, dtype=np.int32)
+    _check(lib().dtp_layout_orders(G, I, L, _ptr(h), _ptr(nu), _ptr(go), _ptr(no)))
+    return go, no
+
+
+WEIGHT_ORDER = ("w_q", "w_k", "w_v", "w_o", "w_gate", "w_up", "w_down")
+
+
+def dtp_apply_layout(d_model, n_neurons, n_q_heads, n_kv_groups, head_dim, dtype, L, h, nu, src,
+                     dst, stream=None):
+    """Permute a layer's weights: ``src`` and ``dst`` map WEIGHT_ORDER names to tensors."""
+    desc = dtp_layer_desc(d_model, n_neurons, n_q_heads, n_kv_groups, head_dim, 0.0, int(dtype))
+    h = np.ascontiguousarray(h, dtype=np.int32)
+    nu = np.ascontiguousarray(nu, dtype=np.int32)
+    srcp = (ctypes.c_void_p * 7)(*[_ptr(src[k]) for k in WEIGHT_ORDER])
+    dstp = (ctypes.c_void_p * 7)(*[_ptr(dst[k]) for k in WEIGHT_ORDER])
+    _check(lib().dtp_apply_layout(ctypes.byref(desc), L, _ptr(h), _ptr(nu),
+                                  ctypes.cast(srcp, ctypes.c_void_p), ctypes.cast(dstp, ctypes.c_void_p),
+                                  _stream(stream)))

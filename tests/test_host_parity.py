@@ -121,3 +121,16 @@ def test_layer_optimum_bit_exact(G, I, L, seed):
     assert J == rJ
     np.testing.assert_array_equal(h, np.array(rh))
     np.testing.assert_array_equal(nu, rnu)
+
+
+# ----------------------------------------------------------------------------- layout orders
+def test_layout_orders_match_oracle():
+    from oracle import apply as ap
+    for (G, I, L, seed) in [(8, 64, 4, 3), (4, 128, 2, 9), (16, 32, 8, 1)]:
+        hs, nus = lay.random_layout(1, G, I, L, seed)
+        go, no = dtp.dtp_layout_orders(G, I, L, hs[0], nus[0])
+        rgo, rno = ap.layout_orders(hs[0], nus[0], L)
+        np.testing.assert_array_equal(go, rgo)
+        np.testing.assert_array_equal(no, rno)
+    with pytest.raises(dtp.DtpError):
+        dtp.dtp_layout_orders(4, 8, 2, np.array([0, 0, 0, 1]), np.zeros(8))
