@@ -89,38 +89,61 @@ def cpu_baseline(wl, x, attn, w, L, n_tokens):
                       f"fp64 folded affinity ({t1 - t0:.1f} s) + exact layout optimiser ({t2 - t1:.1f} s)"}
 
 
-def full_model(dtp, synth, device, torch):
-    """Full-model layout time: every layer's fold + affinity, then encode + ascent."""
-    wl = synth.WORKLOADS["qwen3-0.6b-model"]
-    L = wl.shards[0]
+def full_model(dtp, synth, device, torch, name):
+    """Full-model layout time: every layer's fold + affinity (up edge, and the down edge into
+    the next layer), then encode + ascent to convergence for each shard count."""
+    wl = synth.WORKLOADS[name]
     N, G, I = wl.n_layers, wl.n_kv_groups, wl.n_neurons
     nch = wl.tokens // wl.chunk
-    log(f"full model: generating {N} layers x {wl.tokens} tokens on the device")
-    layers, weights, data = [], [], []
+    dt = dtp.DTP_BF16 if wl.dtype == "bf16" else dtp.DTP_F32
+    log(f"full model {name}: generating {N} layers x {wl.tokens} tokens on the device")
+    layers, weights, attn_w, data = [], [], [], []
     for i in range(N):
         layer, w = make_layer(dtp, synth, wl, i, device)
         layers.append(layer)
         weights.append(w)
-        data.append([synth.device_tokens(wl, i, w, wl.chunk, c, device) for c in range(nch)])
+        attn_w.append(synth.device_attn_weights(wl, i, device))
+        data.append([synth.device_tokens(wl, i, w, wl.chunk, c, device, with_pre=True)
+                     for c in range(nch)])
     A = torch.zeros(N, G, I, dtype=torch.float32, device=device)
+    s_down = torch.zeros(max(N - 1, 1), I, dtype=torch.float32, device=device)
+    B = torch.zeros(G, I, dtype=torch.float32, device=device)
+    A_down = torch.zeros(max(N - 1, 1), I, G, dtype=torch.float32, device=device)
     torch.cuda.synchronize()
-    log("full model: timing")
+    log(f"full model {name}: timing")
     t0 = time.perf_counter()
     for i in range(N):
         w = weights[i]
         dtp.dtp_layer_set_weights(layers[i], w["w_o"], w["gamma"], w["w_gate"], w["w_up"], w["w_down"])
-        for (x, a) in data[i]:
-            dtp.dtp_affinity_accumulate(layers[i], x, a, x.shape[0], A[i])
+        for c, (x, a, _) in enumerate(data[i]):
+            if i + 1 < N:
+                x_next = data[i + 1][c][2]   # residual entering layer i+1's attention pre-norm
+                dtp.dtp_affinity_accumulate_down(layers[i], x, a, x_next, wl.rms_eps, x.shape[0], A[i],
+                                                 s_down[i])
+            else:
+                dtp.dtp_affinity_accumulate(layers[i], x, a, x.shape[0], A[i])
+        if i + 1 < N:
+            an = attn_w[i + 1]
+            dtp.dtp_down_weights(wl.d_model, I, wl.n_q_heads, G, wl.head_dim, dt, an["w_q"], an["w_k"],
+                                 an["w_v"], an["gamma"], w["w_down"], B)
+            dtp.dtp_down_affinity(I, G, s_down[i], B, A_down[i])
     torch.cuda.synchronize()
     t1 = time.perf_counter()
-    res = dtp.dtp_coordinate_ascent(N, G, I, L, A)
-    t2 = time.perf_counter()
+    out = {"workload": wl.name, "layers": N, "tokens_per_layer": wl.tokens, "affinity_s": t1 - t0,
+           "edges": 2 * N - 1, "by_shards": []}
+    for L in wl.shards:
+        ta = time.perf_counter()
+        res = dtp.dtp_coordinate_ascent(N, G, I, L, A, A_down if N > 1 else None)
+        tb = time.perf_counter()
+        out["by_shards"].append({"shards": L, "optimiser_s": tb - ta, "layout_time_s": (t1 - t0) + (tb - ta),
+                                 "sweeps": res["sweeps"], "J": res["J"],
+                                 "J_random_expectation": (2 * N - 1) / L})
     for layer in layers:
         dtp.dtp_layer_destroy(layer)
-    return {"workload": wl.name, "layers": N, "tokens_per_layer": wl.tokens, "shards": L,
-            "layout_time_s": t2 - t0, "affinity_s": t1 - t0, "optimiser_s": t2 - t1,
-            "sweeps": res["sweeps"], "J": res["J"],
-            "context": "paper: affinity pass + optimisation under two minutes per model on one RTX 5090"}
+    del data
+    torch.cuda.empty_cache()
+    out["context"] = "paper: affinity pass + optimisation under two minutes per model on one RTX 5090"
+    return out
 
 
 def main():
@@ -131,7 +154,9 @@ def main():
     ap.add_argument("--workload", default="qwen3-0.6b-layer")
     ap.add_argument("--cpu-sample-tokens", type=int, default=49152)
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--full-model", action="store_true")
+    ap.add_argument("--full-model", nargs="*", default=None, metavar="WORKLOAD",
+                    help="also time the full-model layout (default workloads: "
+                         "qwen3-0.6b-model danube3-500m 8b-class-4layer)")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="only run a plain device copy of this many MiB (HBM counter scale)")
     args = ap.parse_args()
@@ -237,10 +262,11 @@ def main():
         log(f"cpu baseline: oracle on {args.cpu_sample_tokens} tokens")
         out["cpu_baseline"] = cpu_baseline(wl, x, attn, w, L, args.cpu_sample_tokens)
     dtp.dtp_layer_destroy(layer)
-    if args.full_model:
+    if args.full_model is not None:
         del x, attn
         torch.cuda.empty_cache()
-        out["full_model"] = full_model(dtp, synth, device, torch)
+        names = args.full_model or ["qwen3-0.6b-model", "danube3-500m", "8b-class-4layer"]
+        out["full_model"] = [full_model(dtp, synth, device, torch, n) for n in names]
     print(json.dumps(out), flush=True)
 
 
