@@ -159,3 +159,45 @@ def test_down_requires_next_residual():
             dtp.dtp_affinity_accumulate_down(layer, x, a, None, 1e-6, 4, A, A)
     finally:
         dtp.dtp_layer_destroy(layer)
+
+
+def test_chain_layout_with_down_edges_matches_oracle_objective():
+    """A 3-layer chain: up and down affinity from the GPU and from the oracle lead to
+    layouts whose co-located affinity, measured on the oracle's matrices, agrees within
+    1e-3; on the GPU's own matrices the library's ascent equals the oracle's bit for bit."""
+    from oracle import layout as lay
+    wl = synth.shaped(synth.WORKLOADS["qwen3-0.6b-layer"], n_layers=3)
+    N, G, I, L, T = 3, wl.n_kv_groups, wl.n_neurons, 4, 512
+    f = synth.to_f64
+    A_gpu, D_gpu, A_ref, D_ref = [], [], [], []
+    toks = []
+    for i in range(N):
+        w = synth.host_weights(wl, i)
+        toks.append((w,) + synth.host_tokens(wl, i, w, T, with_pre=True))
+    for i in range(N):
+        w, x, a, _ = toks[i]
+        if i + 1 < N:
+            x_next = toks[i + 1][3]
+            an = synth.host_attn_weights(wl, i + 1)
+            A, s, B, S, _ = _gpu(wl, w, x, a, x_next, an)
+            s_ref, B_ref = _oracle(wl, w, x, x_next, an)
+            D_gpu.append(S)
+            D_ref.append(s_ref[:, None] * B_ref.T)
+        else:
+            from tests.helpers import gpu_affinity
+            A = gpu_affinity(wl, w, x, a)
+        A_gpu.append(A)
+        A_ref.append(orc_up.affinity_folded(**oracle_inputs(w, x, a), n_kv_groups=G, eps=wl.rms_eps))
+    res = dtp.dtp_coordinate_ascent(N, G, I, L, torch.from_numpy(np.stack(A_gpu)).cuda(),
+                                    torch.from_numpy(np.stack(D_gpu)).cuda())
+    Qu = [lay.encode(a.astype(np.float32)) for a in A_ref]
+    Qd = [lay.encode(d.astype(np.float32)) for d in D_ref]
+    _, _, J_ref, _ = lay.coordinate_ascent(Qu, Qd, L)
+    J_gpu_layout = lay.objective(Qu, Qd, list(res["h"]), list(res["nu"]))
+    assert abs(J_gpu_layout - J_ref) <= 1e-3 * J_ref
+    hs2, nus2, J2, _ = lay.coordinate_ascent([lay.encode(a) for a in A_gpu],
+                                             [lay.encode(d) for d in D_gpu], L)
+    assert res["J_fixed"] == J2
+    for i in range(N):
+        np.testing.assert_array_equal(res["h"][i], np.array(hs2[i]))
+        np.testing.assert_array_equal(res["nu"][i], nus2[i])
