@@ -6,6 +6,7 @@
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
+#include <mutex>
 #include <thread>
 
 #include "dtp_internal.h"
@@ -113,14 +114,39 @@ void shuffle(int32_t* a, int n, uint64_t seed, uint64_t* counter) {
   }
 }
 
+// Stream-ordered scratch released on the stream it was allocated on.
 struct DevBuf {
   void* p = nullptr;
+  hipStream_t s = nullptr;
+  explicit DevBuf(hipStream_t stream) : s(stream) {}
   ~DevBuf() {
-    if (p) (void)hipFree(p);
+    if (p) (void)stream_free(p, s);
   }
 };
 
 }  // namespace
+
+hipError_t stream_alloc(void** p, size_t bytes, hipStream_t s) {
+  static std::mutex mu;
+  static bool retained[64] = {};
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev >= 0 && dev < 64) {
+    std::lock_guard<std::mutex> lock(mu);
+    if (!retained[dev]) {
+      hipMemPool_t pool;
+      if (hipDeviceGetDefaultMemPool(&pool, dev) == hipSuccess) {
+        uint64_t keep = UINT64_MAX;
+        (void)hipMemPoolSetAttribute(pool, hipMemPoolAttrReleaseThreshold, &keep);
+      }
+      retained[dev] = true;
+    }
+  }
+  return hipMallocAsync(p, bytes, s);
+}
+
+hipError_t stream_free(void* p, hipStream_t s) { return hipFreeAsync(p, s); }
 }  // namespace dtp
 
 using namespace dtp;
@@ -199,20 +225,20 @@ dtp_status dtp_partition_scores(int32_t G, int32_t I, int32_t L, const int64_t* 
   // as its incoming down edge.  Without a down edge one layer suffices.
   const bool down = Q_down_prev != nullptr;
   ScoreWorkspace ws;
-  st = score_workspace_create(&ws, down ? 2 : 1, G, I, L);
+  st = score_workspace_create(&ws, down ? 2 : 1, G, I, L, s);
   if (st != DTP_OK) {
     score_workspace_destroy(&ws);
     return st;
   }
-  DevBuf qbuf, nbuf;
+  DevBuf qbuf(s), nbuf(s);
   const int64_t* qu = Q_up;
   const int32_t* nl = nu;
   if (down) {
     // layer 0 gets zero codes; layer 1 is the real layer
     const size_t qbytes = sizeof(int64_t) * (size_t)G * I;
     const size_t nbytes = sizeof(int32_t) * (size_t)I;
-    hipError_t e = hipMalloc(&qbuf.p, 2 * qbytes);
-    if (e == hipSuccess) e = hipMalloc(&nbuf.p, 2 * nbytes);
+    hipError_t e = stream_alloc(&qbuf.p, 2 * qbytes, s);
+    if (e == hipSuccess) e = stream_alloc(&nbuf.p, 2 * nbytes, s);
     if (e == hipSuccess) e = hipMemsetAsync(qbuf.p, 0, qbytes, s);
     if (e == hipSuccess)
       e = hipMemcpyAsync((char*)qbuf.p + qbytes, Q_up, qbytes, hipMemcpyDeviceToDevice, s);
@@ -280,7 +306,7 @@ dtp_status dtp_coordinate_ascent(int32_t N, int32_t G, int32_t I, int32_t L, con
 
   // Device copies of the codes for the head step.
   ScoreWorkspace ws;
-  st = score_workspace_create(&ws, N, G, I, L);
+  st = score_workspace_create(&ws, N, G, I, L, s);
   if (st != DTP_OK) {
     score_workspace_destroy(&ws);
     return st;
@@ -290,9 +316,9 @@ dtp_status dtp_coordinate_ascent(int32_t N, int32_t G, int32_t I, int32_t L, con
     ~WsGuard() { score_workspace_destroy(w); }
   } guard{&ws};
   // One device block for the codes and the neuron assignments: [Q_up | Q_down | nu].
-  DevBuf block;
+  DevBuf block(s);
   const size_t qu_bytes = sizeof(int64_t) * nup, qd_bytes = sizeof(int64_t) * ndown;
-  DTP_HIP(hipMalloc(&block.p, qu_bytes + qd_bytes + sizeof(int32_t) * (size_t)N * I));
+  DTP_HIP(stream_alloc(&block.p, qu_bytes + qd_bytes + sizeof(int32_t) * (size_t)N * I, s));
   int64_t* qu_dev = (int64_t*)block.p;
   int64_t* qd_dev = has_down ? qu_dev + nup : nullptr;
   int32_t* nu_dev = (int32_t*)((char*)block.p + qu_bytes + qd_bytes);
@@ -355,6 +381,8 @@ dtp_status dtp_coordinate_ascent(int32_t N, int32_t G, int32_t I, int32_t L, con
     J_prev = Jc;
     if (!improved) break;
   }
+  // The uploads read host vectors that die on return.
+  DTP_HIP(hipStreamSynchronize(s));
   std::memcpy(h, hs.data(), sizeof(int32_t) * hs.size());
   std::memcpy(nu, nus.data(), sizeof(int32_t) * nus.size());
   *J_fixed = J_prev;

@@ -19,7 +19,7 @@
 //   prep_gate_up_kernel   W' = W diag(gamma), gate and up rows interleaved per neuron tile
 //   transpose_kernel      W_o^T, so both fold operands are K-contiguous
 //   fold_kernel           F = W' W_o (MFMA)
-//   down_norm_kernel      n_d[k] = ||w^d_k||^2
+//   down_norm_*_kernel    n_d[k] = ||w^d_k||^2 (row chunks, then their fixed-order sum)
 //   rms_kernel            1/r per token
 //   affinity_bf16_kernel  the fused operating point + per-head damage + token reduction
 //   reduce_splits_kernel  deterministic fp64 sum of the per-split partials into A
@@ -76,6 +76,34 @@ __global__ void prep_gate_up_kernel(const T* __restrict__ w_gate, const T* __res
       out[rowi * ld + j] = f32_to_bf16(v);
     else
       out[rowi * ld + j] = v;
+  }
+}
+
+// bf16 version of the above, eight columns per thread (d % 8 == 0): 16-byte loads and stores.
+__global__ void prep_gate_up_bf16x8_kernel(const uint16_t* __restrict__ w_gate,
+                                           const uint16_t* __restrict__ w_up,
+                                           const uint16_t* __restrict__ gamma, int I, int d,
+                                           int n_tiles, int64_t ld, uint16_t* __restrict__ out) {
+  const int d8 = d / 8;
+  const int64_t total = (int64_t)n_tiles * kCols * d8;
+  for (int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; idx < total;
+       idx += (int64_t)gridDim.x * blockDim.x) {
+    const int j = (int)(idx % d8) * 8;
+    const int64_t rowi = idx / d8;
+    const int c = (int)(rowi % kCols);
+    const int k = (int)(rowi / kCols) * kBN + (c % kBN);
+    u32x4 o = {0u, 0u, 0u, 0u};
+    if (k < I) {
+      const u32x4 w = *reinterpret_cast<const u32x4*>((c < kBN ? w_gate : w_up) + (int64_t)k * d + j);
+      const u32x4 g = *reinterpret_cast<const u32x4*>(gamma + j);
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const float lo = __uint_as_float(w[e] << 16) * __uint_as_float(g[e] << 16);
+        const float hi = __uint_as_float(w[e] & 0xffff0000u) * __uint_as_float(g[e] & 0xffff0000u);
+        o[e] = (uint32_t)f32_to_bf16(lo) | ((uint32_t)f32_to_bf16(hi) << 16);
+      }
+    }
+    *reinterpret_cast<u32x4*>(out + rowi * ld + j) = o;
   }
 }
 
@@ -161,27 +189,32 @@ __global__ void fold_f32_kernel(const float* __restrict__ w_o, const float* __re
   }
 }
 
-// nd[k] = sum_j w_down[j][k]^2.  Block = 64 columns x 16 row groups; the row groups'
-// partial sums are added in a fixed order.
+// nd[k] = sum_j w_down[j][k]^2 in two passes: part[c][k] sums the rows of chunk c (one
+// thread per chunk and column, coalesced across columns), then the chunks are added in order.
 template <typename T>
-__global__ void __launch_bounds__(1024)
-down_norm_kernel(const T* __restrict__ w_down, int d, int I, int I_pad, float* __restrict__ nd) {
-  __shared__ float part[16][64];
-  const int c = threadIdx.x & 63, rg = threadIdx.x >> 6;
-  const int k = blockIdx.x * 64 + c;
+__global__ void __launch_bounds__(256)
+down_norm_part_kernel(const T* __restrict__ w_down, int d, int I, int chunk_rows,
+                      float* __restrict__ part) {
+  const int k = blockIdx.x * 256 + threadIdx.x;
+  const int c = blockIdx.y;
+  if (k >= I) return;
+  const int j1 = min(d, (c + 1) * chunk_rows);
   float s = 0.0f;
-  if (k < I)
-    for (int j = rg; j < d; j += 16) {
-      const float v = load_f32(w_down, (int64_t)j * I + k);
-      s = fmaf(v, v, s);
-    }
-  part[rg][c] = s;
-  __syncthreads();
-  if (rg == 0 && k < I_pad) {
-    float t = 0.0f;
-    for (int r = 0; r < 16; ++r) t += part[r][c];
-    nd[k] = t;
+  for (int j = c * chunk_rows; j < j1; ++j) {
+    const float v = load_f32(w_down, (int64_t)j * I + k);
+    s = fmaf(v, v, s);
   }
+  part[(int64_t)c * I + k] = s;
+}
+
+__global__ void down_norm_sum_kernel(const float* __restrict__ part, int chunks, int I, int I_pad,
+                                     float* __restrict__ nd) {
+  const int k = blockIdx.x * blockDim.x + threadIdx.x;
+  if (k >= I_pad) return;
+  double t = 0.0;
+  if (k < I)
+    for (int c = 0; c < chunks; ++c) t += (double)part[(int64_t)c * I + k];
+  nd[k] = (float)t;
 }
 
 // ------------------------------------------------------------------ per-token scalars
@@ -749,19 +782,29 @@ affinity_f32_kernel(AffinityF32Args p) {
   }
 }
 
-// A[g][k] += sum_s partial[s][g][k] for g < G, and s_down[k] += sum_s partial[s][G][k] when
-// s_down is given, in fp64 and in split order.
-__global__ void reduce_splits_kernel(const float* __restrict__ partial, int splits, int G, int I,
-                                     int I_pad, float* __restrict__ A, float* __restrict__ s_down) {
-  const int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  const int rows = s_down ? G + 1 : G;
-  if (idx >= (int64_t)rows * I) return;
-  const int g = (int)(idx / I), k = (int)(idx % I);
-  float* out = g < G ? A + idx : s_down + k;
-  double s = (double)*out;
-  for (int sp = 0; sp < splits; ++sp)
-    s += (double)partial[((int64_t)sp * (G + 1) + g) * I_pad + k];
-  *out = (float)s;
+// A[g][k] += sum_s partial[s][g][k] for g < G (row g = blockIdx.y), and s_down[k] +=
+// sum_s partial[s][G][k] when s_down is given, in fp64 and in a fixed order: eight split
+// groups (splits r, r + 8, r + 16, ...) summed in parallel, then the groups in order.
+constexpr int kReduceGroups = 8;
+__global__ void __launch_bounds__(256)
+reduce_splits_kernel(const float* __restrict__ partial, int splits, int G, int I, int I_pad,
+                     float* __restrict__ A, float* __restrict__ s_down) {
+  __shared__ double part[kReduceGroups][32];
+  const int kk = threadIdx.x & 31, r = threadIdx.x >> 5;
+  const int g = blockIdx.y;
+  const int k = blockIdx.x * 32 + kk;
+  double s = 0.0;
+  if (k < I)
+    for (int sp = r; sp < splits; sp += kReduceGroups)
+      s += (double)partial[((int64_t)sp * (G + 1) + g) * I_pad + k];
+  part[r][kk] = s;
+  __syncthreads();
+  if (r == 0 && k < I) {
+    float* out = g < G ? A + (int64_t)g * I + k : s_down + k;
+    double t = (double)*out;
+    for (int q = 0; q < kReduceGroups; ++q) t += part[q][kk];
+    *out = (float)t;
+  }
 }
 
 inline unsigned grid_for(int64_t n, int threads) {
@@ -805,6 +848,24 @@ void layer_free(dtp_layer L) {
     (void)hipEventDestroy(e.second);
   }
   delete L;
+}
+
+// n_d into L->nd, with the layer's split partials as the scratch of the row chunks (the
+// affinity launches that use them are ordered after this on the stream).
+template <typename T>
+dtp_status down_norms(const T* w_down, dtp_layer L, hipStream_t s) {
+  const dtp_layer_desc& d = L->desc;
+  const int64_t cap = (int64_t)kMaxSplits * (d.n_kv_groups + 1) * L->I_pad;  // floats
+  int chunk_rows = 32;
+  while ((int64_t)((d.d_model + chunk_rows - 1) / chunk_rows) * d.n_neurons > cap) chunk_rows *= 2;
+  const int chunks = (d.d_model + chunk_rows - 1) / chunk_rows;
+  down_norm_part_kernel<T><<<dim3((d.n_neurons + 255) / 256, chunks), 256, 0, s>>>(
+      w_down, d.d_model, d.n_neurons, chunk_rows, L->partial);
+  DTP_HIP(hipGetLastError());
+  down_norm_sum_kernel<<<(L->I_pad + 255) / 256, 256, 0, s>>>(L->partial, chunks, d.n_neurons,
+                                                               L->I_pad, L->nd);
+  DTP_HIP(hipGetLastError());
+  return DTP_OK;
 }
 
 dtp_status check_device(dtp_layer L) {
@@ -949,7 +1010,7 @@ dtp_status accumulate(dtp_layer L, const void* x, const void* attn, const void* 
       DTP_HIP(hipEventRecord(e1, s));
       L->events.emplace_back(e0, e1);
     }
-    reduce_splits_kernel<<<grid_for((int64_t)(G + 1) * I, 256), 256, 0, s>>>(
+    reduce_splits_kernel<<<dim3((I + 31) / 32, s_down ? G + 1 : G), 256, 0, s>>>(
         L->partial, splits, G, I, L->I_pad, A, s_down);
     DTP_HIP(hipGetLastError());
   }
@@ -1038,9 +1099,14 @@ dtp_status dtp_layer_set_weights(dtp_layer L, const void* w_o, const void* gamma
   const int H = d.n_q_heads, dh = d.head_dim, HD = H * dh, I = d.n_neurons, dm = d.d_model;
   const int64_t n = (int64_t)L->n_tiles * kCols * dm;
   if (d.dtype == DTP_BF16) {
-    prep_gate_up_kernel<uint16_t><<<grid_for(n, 256), 256, 0, s>>>(
-        (const uint16_t*)w_gate, (const uint16_t*)w_up, (const uint16_t*)gamma, I, dm, L->n_tiles,
-        L->Kt, (uint16_t*)L->w);
+    if (aligned16(w_gate) && aligned16(w_up) && aligned16(gamma))
+      prep_gate_up_bf16x8_kernel<<<grid_for(n / 8, 256), 256, 0, s>>>(
+          (const uint16_t*)w_gate, (const uint16_t*)w_up, (const uint16_t*)gamma, I, dm,
+          L->n_tiles, L->Kt, (uint16_t*)L->w);
+    else
+      prep_gate_up_kernel<uint16_t><<<grid_for(n, 256), 256, 0, s>>>(
+          (const uint16_t*)w_gate, (const uint16_t*)w_up, (const uint16_t*)gamma, I, dm,
+          L->n_tiles, L->Kt, (uint16_t*)L->w);
     DTP_HIP(hipGetLastError());
     dim3 tg((HD + 31) / 32, (dm + 31) / 32);
     transpose_kernel<<<tg, 256, 0, s>>>((const uint16_t*)w_o, dm, HD, (uint16_t*)L->woT);
@@ -1048,9 +1114,8 @@ dtp_status dtp_layer_set_weights(dtp_layer L, const void* w_o, const void* gamma
     dim3 fg(L->n_tiles * kCols / kBM, (HD + kCols - 1) / kCols);
     fold_kernel<<<fg, kThreads, 0, s>>>((uint16_t*)L->w, (const uint16_t*)L->woT, HD, dm, L->Kt);
     DTP_HIP(hipGetLastError());
-    down_norm_kernel<uint16_t><<<L->I_pad / 64, 1024, 0, s>>>((const uint16_t*)w_down, dm, I,
-                                                             L->I_pad, L->nd);
-    DTP_HIP(hipGetLastError());
+    st = down_norms((const uint16_t*)w_down, L, s);
+    if (st != DTP_OK) return st;
   } else {
     prep_gate_up_kernel<float><<<grid_for(n, 256), 256, 0, s>>>(
         (const float*)w_gate, (const float*)w_up, (const float*)gamma, I, dm, L->n_tiles, dm,
@@ -1061,9 +1126,8 @@ dtp_status dtp_layer_set_weights(dtp_layer L, const void* w_o, const void* gamma
                                                        (const float*)w_gate, (const float*)w_up,
                                                        dm, I, H, dh, L->fold32);
     DTP_HIP(hipGetLastError());
-    down_norm_kernel<float><<<L->I_pad / 64, 1024, 0, s>>>((const float*)w_down, dm, I, L->I_pad,
-                                                           L->nd);
-    DTP_HIP(hipGetLastError());
+    st = down_norms((const float*)w_down, L, s);
+    if (st != DTP_OK) return st;
   }
   L->has_weights = true;
   return DTP_OK;

@@ -35,6 +35,12 @@ constexpr int64_t kMaxPartitions = int64_t(1) << 24;
 constexpr int kFracBits = 48;
 constexpr int kMantBits = 40;
 
+// ---- stream-ordered scratch (abi.cpp): hipMallocAsync / hipFreeAsync from the device's
+// default pool, which is told once per device to keep freed memory, so per-call scratch
+// costs neither a device-wide synchronisation nor a trip to the driver.
+hipError_t stream_alloc(void** p, size_t bytes, hipStream_t s);
+hipError_t stream_free(void* p, hipStream_t s);
+
 // ---- unit-mass fixed point (encode.cpp)
 dtp_status encode_unit_mass(const float* A, int64_t n, int64_t* Q);
 
@@ -51,12 +57,14 @@ void balanced_assign_exact(int I, int L, const int64_t* M, int32_t* nu, int64_t*
 struct ScoreWorkspace {
   int N = 0, G = 0, I = 0, L = 0;
   int64_t P = 0;
+  hipStream_t stream = nullptr;    // the allocation and its release are ordered on it
+  std::vector<uint8_t> host_table;  // source of the table upload, kept until release
   uint8_t* table = nullptr;   // dev [P][G]
   int64_t* C = nullptr;       // dev [N][G][L]
   int64_t* scores = nullptr;  // dev [N][P]
   int64_t* best = nullptr;    // dev [N]
 };
-dtp_status score_workspace_create(ScoreWorkspace* ws, int N, int G, int I, int L);
+dtp_status score_workspace_create(ScoreWorkspace* ws, int N, int G, int I, int L, hipStream_t s);
 void score_workspace_destroy(ScoreWorkspace* ws);
 // Q_up dev [N][G][I]; nu dev [N][I]; Q_down dev [N-1][I][G] or null (layer i uses
 // Q_down[i-1] with nu[i-1]).  Enqueues C, scores and best on `stream`.

@@ -115,7 +115,8 @@ best_partition_kernel(const int64_t* __restrict__ scores, int64_t P, int minimis
 
 }  // namespace
 
-dtp_status score_workspace_create(ScoreWorkspace* ws, int N, int G, int I, int L) {
+dtp_status score_workspace_create(ScoreWorkspace* ws, int N, int G, int I, int L, hipStream_t s) {
+  ws->stream = s;
   ws->N = N;
   ws->G = G;
   ws->I = I;
@@ -124,24 +125,26 @@ dtp_status score_workspace_create(ScoreWorkspace* ws, int N, int G, int I, int L
   DTP_CHECK(ws->P > 0 && ws->P <= kMaxPartitions, DTP_ERR_UNSUPPORTED,
             "%lld partitions of %d groups over %d devices exceed the limit of %lld",
             (long long)ws->P, G, L, (long long)kMaxPartitions);
-  const std::vector<uint8_t> table = enumerate_partitions(G, L);
+  ws->host_table = enumerate_partitions(G, L);
+  const std::vector<uint8_t>& table = ws->host_table;
   // One allocation: [C | scores | best | table], each part 256-byte aligned.
   auto up = [](size_t b) { return (b + 255) & ~size_t(255); };
   const size_t c_bytes = up(sizeof(int64_t) * (size_t)N * G * L);
   const size_t s_bytes = up(sizeof(int64_t) * (size_t)N * ws->P);
   const size_t b_bytes = up(sizeof(int64_t) * (size_t)N);
   char* base = nullptr;
-  DTP_HIP(hipMalloc(&base, c_bytes + s_bytes + b_bytes + table.size()));
+  DTP_HIP(stream_alloc((void**)&base, c_bytes + s_bytes + b_bytes + table.size(), s));
   ws->C = (int64_t*)base;
   ws->scores = (int64_t*)(base + c_bytes);
   ws->best = (int64_t*)(base + c_bytes + s_bytes);
   ws->table = (uint8_t*)(base + c_bytes + s_bytes + b_bytes);
-  DTP_HIP(hipMemcpy(ws->table, table.data(), table.size(), hipMemcpyHostToDevice));
+  DTP_HIP(hipMemcpyAsync(ws->table, table.data(), table.size(), hipMemcpyHostToDevice, s));
   return DTP_OK;
 }
 
+// The host table must outlive its upload: callers synchronise the stream before this.
 void score_workspace_destroy(ScoreWorkspace* ws) {
-  if (ws->C) (void)hipFree(ws->C);
+  if (ws->C) (void)stream_free(ws->C, ws->stream);
   *ws = ScoreWorkspace();
 }
 
