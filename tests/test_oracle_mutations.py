@@ -172,3 +172,61 @@ def test_optimum_over_contiguous_heads_only_is_caught(monkeypatch):
     monkeypatch.setattr(lay, "unlabelled_partitions", lambda G, L: [lay.contiguous_heads(G, L)])
     with pytest.raises(AssertionError):
         pl.test_layer_optimum_equals_brute_force(4, 8, 2, 31)
+
+
+# ---- the paper's approximate neuron assignment
+from oracle import dual_ascent as da  # noqa: E402
+from tests import test_oracle_dual_ascent as pda  # noqa: E402
+
+
+def test_one_sided_swap_gain_is_caught(monkeypatch):
+    def bad(M, nu):
+        _, L = M.shape
+        nu = np.array(nu, dtype=np.int64)
+        for a in range(L):
+            for b in range(a + 1, L):
+                on_a, on_b = np.flatnonzero(nu == a), np.flatnonzero(nu == b)
+                to_b = M[on_a, b] - M[on_a, a]
+                i = int(np.argmax(to_b))
+                if to_b[i] > 0:   # ignores what the partner loses
+                    j = int(np.argmin(M[on_b, b] - M[on_b, a]))
+                    nu[on_a[i]], nu[on_b[j]] = b, a
+        return nu
+    monkeypatch.setattr(da, "pairwise_swaps", bad)
+    with pytest.raises(AssertionError):
+        pda.test_swaps_from_the_contiguous_layout_end_at_a_local_optimum(24, 3, 11)
+
+
+def test_costliest_fix_up_move_is_caught(monkeypatch):
+    def bad(M, nu):
+        I, L = M.shape
+        cap = I // L
+        nu = np.array(nu, dtype=np.int64)
+        load = np.bincount(nu, minlength=L)
+        while np.any(load > cap):
+            movable = np.flatnonzero(load[nu] > cap)
+            targets = np.flatnonzero(load < cap)
+            loss = M[movable, nu[movable]][:, None] - M[np.ix_(movable, targets)]
+            flat = int(np.argmax(loss))
+            k, b = movable[flat // len(targets)], targets[flat % len(targets)]
+            load[nu[k]] -= 1
+            load[b] += 1
+            nu[k] = b
+        return nu
+    monkeypatch.setattr(da, "fix_up", bad)
+    with pytest.raises(AssertionError):
+        pda.test_fix_up_moves_the_cheapest_excess()
+
+
+def test_offsets_moving_the_wrong_way_are_caught(monkeypatch):
+    orig = da.dual_offsets
+
+    def bad(M, iterations=da.ITERATIONS, decay=da.DECAY):
+        lam, _ = orig(M, iterations, decay)
+        lam = -lam
+        return lam, np.argmax(M.astype(np.float64) - lam[None, :], axis=1)
+    monkeypatch.setattr(da, "dual_offsets", bad)
+    M = np.zeros((12, 3), dtype=np.int64)
+    M[:, 0] = 10          # every neuron prefers device 0: the offsets must push them away
+    lam, _ = da.dual_offsets(M)
+    assert lam[0] < 0     # wrong direction: device 0 got cheaper
