@@ -221,6 +221,16 @@ def main():
     t1 = time.perf_counter()
     kern_ms, launches = dtp.dtp_layer_profile_read(layer)
     dtp.dtp_layer_profile(layer, 0)
+    # The paper's approximate neuron step against the exact one, on this layer's affinity
+    # (untimed): J of the ascent with each, at the workload's shard count and at L = 4.
+    neuron_steps = {}
+    for Ls in sorted({L, 4}):
+        if G % Ls or I % Ls:
+            continue
+        ex = dtp.dtp_coordinate_ascent(1, G, I, Ls, A)
+        du = dtp.dtp_coordinate_ascent(1, G, I, Ls, A, dual_ascent_neurons=True)
+        neuron_steps[f"L{Ls}"] = {"J_exact": ex["J"], "J_dual_ascent": du["J"],
+                                  "relative_gap": (ex["J"] - du["J"]) / ex["J"]}
     ms_per_step = (t1 - t0) * 1e3 / args.steps
     value = T / (ms_per_step * 1e-3)
     # The library splits a call into slices, one kernel launch each: the algorithmic work
@@ -255,7 +265,7 @@ def main():
         "step_tflops": flops_per_token(wl) * T / (ms_per_step * 1e-3) / 1e12,
         "breakdown_ms": {"fold": (b1 - b0) * 1e3, "affinity": (b2 - b1) * 1e3,
                          "layout": (b3 - b2) * 1e3},
-        "layout": {"J": res["J"], "sweeps": res["sweeps"]},
+        "layout": {"J": res["J"], "sweeps": res["sweeps"], "neuron_step": neuron_steps},
         "context": "paper: 65,536-token affinity pass of a 28-layer model in 51 s on one RTX 5090",
     }
     if not args.no_cpu_baseline:

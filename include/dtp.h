@@ -195,16 +195,34 @@ dtp_status dtp_balanced_assign(int32_t G, int32_t I, int32_t L, const int64_t* Q
                                const int32_t* h, const int64_t* Q_down, const int32_t* h_next,
                                int32_t minimise, int32_t* nu, int64_t* value);
 
+/* The same neuron step solved the way the paper does (Section 3, "Optimiser"; 300
+ * iterations with step decay 0.98 from the appendix), kept to measure its distance from the
+ * optimum: dual ascent on L device offsets (from zero, first step (max M - min M) / I; each
+ * neuron takes argmax_l M[k, l] - lambda_l, lowest l on ties, and lambda_l rises by
+ * step * (load_l - I/L)), then a fix-up that moves the cheapest neurons from overloaded to
+ * underloaded devices one at a time, then pairwise swaps (device pairs in order, the best
+ * exchange per pair when its total gain is positive) until a full scan exchanges nothing.
+ * Balanced; value <= dtp_balanced_assign's; equal to it when L = 2.  Same arguments, sizes
+ * and errors as dtp_balanced_assign.  Host only. */
+dtp_status dtp_balanced_assign_dual_ascent(int32_t G, int32_t I, int32_t L, const int64_t* Q_up,
+                                           const int32_t* h, const int64_t* Q_down,
+                                           const int32_t* h_next, int32_t minimise, int32_t* nu,
+                                           int64_t* value);
+
 /* Options of the coordinate ascent; NULL means the defaults
- * {max_sweeps = 64, freeze_heads = 0, freeze_neurons = 0, minimise = 0, layer_mask = NULL}.
+ * {max_sweeps = 64, freeze_heads = 0, freeze_neurons = 0, minimise = 0, layer_mask = NULL,
+ *  dual_ascent_neurons = 0}.
  * freeze_*: keep that block at its contiguous start.  layer_mask (host [N] or NULL): a zero
- * entry keeps layer i contiguous.  minimise: minimise J instead (anti-optimised layouts). */
+ * entry keeps layer i contiguous.  minimise: minimise J instead (anti-optimised layouts).
+ * dual_ascent_neurons: solve the neuron step with the paper's approximate method
+ * (dtp_balanced_assign_dual_ascent) instead of exactly. */
 typedef struct {
   int32_t max_sweeps;
   int32_t freeze_heads;
   int32_t freeze_neurons;
   int32_t minimise;
   const uint8_t* layer_mask;
+  int32_t dual_ascent_neurons;
 } dtp_ca_options;
 
 /* Coordinate ascent over a chain of N layers (Section 3, "Optimiser"): start from the

@@ -263,11 +263,13 @@ def objective(Q_up: list, Q_down: list, hs: list, nus: list) -> int:
 
 def coordinate_ascent(Q_up: list, Q_down, L: int, max_sweeps: int = 64,
                       freeze_heads: bool = False, freeze_neurons: bool = False,
-                      minimise: bool = False, layer_mask=None):
+                      minimise: bool = False, layer_mask=None, neuron_step=None):
     """Alternate the neuron and head blocks from contiguous layouts (Section 3, Optimiser).
 
     Returns (hs, nus, J_int, sweeps).  ``layer_mask[i]`` false keeps layer i contiguous;
     ``freeze_*`` keep that block contiguous; ``minimise`` minimises J instead.
+    ``neuron_step(M, minimise) -> nu`` replaces the exact neuron step (default: the
+    canonical optimum of ``balanced_assign``).
     """
     N = len(Q_up)
     G, I = Q_up[0].shape
@@ -285,7 +287,10 @@ def coordinate_ascent(Q_up: list, Q_down, L: int, max_sweeps: int = 64,
                     continue
                 down = Q_down[i] if (Q_down is not None and i + 1 < N) else None
                 M = neuron_gain(Q_up[i], hs[i], L, down, hs[i + 1] if down is not None else None)
-                nus[i], _ = balanced_assign(M, minimise)
+                if neuron_step is None:
+                    nus[i], _ = balanced_assign(M, minimise)
+                else:
+                    nus[i] = np.asarray(neuron_step(M, minimise))
         if not freeze_heads:
             for i in range(N):
                 if not moves[i]:

@@ -207,6 +207,26 @@ dtp_status dtp_balanced_assign(int32_t G, int32_t I, int32_t L, const int64_t* Q
   return DTP_OK;
 }
 
+dtp_status dtp_balanced_assign_dual_ascent(int32_t G, int32_t I, int32_t L, const int64_t* Q_up,
+                                           const int32_t* h, const int64_t* Q_down,
+                                           const int32_t* h_next, int32_t minimise, int32_t* nu,
+                                           int64_t* value) {
+  clear_error();
+  dtp_status st = check_layout_sizes(G, I, L, kMaxAssignDevices);
+  if (st != DTP_OK) return st;
+  DTP_CHECK(Q_up && h && nu && value, DTP_ERR_INVALID_ARG, "a required pointer is NULL");
+  DTP_CHECK((Q_down == nullptr) == (h_next == nullptr), DTP_ERR_INVALID_ARG,
+            "Q_down and h_next must both be given or both be NULL");
+  if ((st = check_balanced(h, G, L, "h")) != DTP_OK) return st;
+  if (h_next && (st = check_balanced(h_next, G, L, "h_next")) != DTP_OK) return st;
+  std::vector<int64_t> M;
+  neuron_gain(G, I, L, Q_up, h, Q_down, h_next, minimise != 0, &M);
+  int64_t v = 0;
+  balanced_assign_dual_ascent(I, L, M.data(), kDualAscentIterations, kDualAscentDecay, nu, &v);
+  *value = minimise ? -v : v;
+  return DTP_OK;
+}
+
 dtp_status dtp_partition_scores(int32_t G, int32_t I, int32_t L, const int64_t* Q_up,
                                 const int32_t* nu, const int64_t* Q_down_prev,
                                 const int32_t* nu_prev, int32_t minimise, int64_t* scores,
@@ -277,7 +297,7 @@ dtp_status dtp_coordinate_ascent(int32_t N, int32_t G, int32_t I, int32_t L, con
   DTP_CHECK(A_up && h && nu && J_fixed && J && sweeps, DTP_ERR_INVALID_ARG,
             "a required pointer is NULL");
   DTP_CHECK(A_down == nullptr || N >= 2, DTP_ERR_INVALID_ARG, "A_down needs N >= 2");
-  dtp_ca_options opt = {64, 0, 0, 0, nullptr};
+  dtp_ca_options opt = {64, 0, 0, 0, nullptr, 0};
   if (options) opt = *options;
   DTP_CHECK(opt.max_sweeps >= 1, DTP_ERR_INVALID_ARG, "max_sweeps=%d must be >= 1",
             opt.max_sweeps);
@@ -351,7 +371,11 @@ dtp_status dtp_coordinate_ascent(int32_t N, int32_t G, int32_t I, int32_t L, con
           neuron_gain(G, I, L, Qu.data() + (size_t)i * G * I, hs.data() + (size_t)i * G,
                       dn ? Qd.data() + (size_t)i * I * G : nullptr,
                       dn ? hs.data() + (size_t)(i + 1) * G : nullptr, minimise, &M);
-          balanced_assign_exact(I, L, M.data(), nus.data() + (size_t)i * I, nullptr);
+          if (opt.dual_ascent_neurons)
+            balanced_assign_dual_ascent(I, L, M.data(), kDualAscentIterations, kDualAscentDecay,
+                                        nus.data() + (size_t)i * I, nullptr);
+          else
+            balanced_assign_exact(I, L, M.data(), nus.data() + (size_t)i * I, nullptr);
         }
       };
       if (nthreads == 1) {

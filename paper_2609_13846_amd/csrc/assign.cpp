@@ -213,4 +213,117 @@ void balanced_assign_exact(int I, int L, const int64_t* M, int32_t* nu_out, int6
   if (value) *value = v;
 }
 
+// ------------------------------------------------------------------ the paper's heuristic
+// The approximate solver the paper uses for the same problem (Section 3, "Optimiser", and
+// the appendix's 300 iterations with step decay 0.98), kept to measure its distance from
+// the optimum:
+// 1. Dual ascent on device offsets lambda (starting at 0, first step (max M - min M) / I):
+//    every neuron takes argmax_l (M[k][l] - lambda_l), lowest l on ties, and each device's
+//    offset rises by step * (load_l - I/L); the step is multiplied by the decay.
+// 2. Fix-up: from the assignment the final offsets induce, move one neuron at a time from
+//    an overloaded device to an underloaded one, the move losing the least gain first
+//    (smallest neuron, then smallest device, on ties).
+// 3. Pairwise swaps: scan device pairs (a, b), a < b; exchange the neuron of a gaining most
+//    by moving to b with the neuron of b gaining most by moving to a (smallest indices on
+//    ties) when the two gains sum to more than zero; repeat until a scan exchanges nothing.
+// The offsets are doubles: M's entries are exact in fp64 below 2^53.  Each update is a
+// product and then a sum in separate statements, so no fused multiply-add changes it.
+void balanced_assign_dual_ascent(int I, int L, const int64_t* M, int iterations, double decay,
+                                 int32_t* nu_out, int64_t* value) {
+  const int cap = I / L;
+  std::vector<double> lam(L, 0.0);
+  int64_t lo = M[0], hi = M[0];
+  for (int64_t i = 0; i < (int64_t)I * L; ++i) {
+    lo = std::min(lo, M[i]);
+    hi = std::max(hi, M[i]);
+  }
+  double step = ((double)hi - (double)lo) / (double)I;
+  std::vector<int32_t> nu(I);
+  std::vector<int> load(L);
+  auto induce = [&]() {
+    std::fill(load.begin(), load.end(), 0);
+    for (int k = 0; k < I; ++k) {
+      int best = 0;
+      double bv = (double)M[(size_t)k * L] - lam[0];
+      for (int l = 1; l < L; ++l) {
+        const double v = (double)M[(size_t)k * L + l] - lam[l];
+        if (v > bv) {
+          bv = v;
+          best = l;
+        }
+      }
+      nu[k] = best;
+      ++load[best];
+    }
+  };
+  for (int it = 0; it < iterations; ++it) {
+    induce();
+    for (int l = 0; l < L; ++l) {
+      const double inc = step * (double)(load[l] - cap);
+      lam[l] = lam[l] + inc;
+    }
+    step = step * decay;
+  }
+  induce();
+  // fix-up
+  for (;;) {
+    bool over = false;
+    for (int l = 0; l < L; ++l) over = over || load[l] > cap;
+    if (!over) break;
+    int64_t best_loss = 0;
+    int bk = -1, bb = -1;
+    for (int k = 0; k < I; ++k) {
+      const int a = nu[k];
+      if (load[a] <= cap) continue;
+      for (int b = 0; b < L; ++b) {
+        if (load[b] >= cap) continue;
+        const int64_t loss = M[(size_t)k * L + a] - M[(size_t)k * L + b];
+        if (bk < 0 || loss < best_loss) {
+          best_loss = loss;
+          bk = k;
+          bb = b;
+        }
+      }
+    }
+    --load[nu[bk]];
+    ++load[bb];
+    nu[bk] = bb;
+  }
+  // pairwise swaps
+  for (bool changed = true; changed;) {
+    changed = false;
+    for (int a = 0; a < L; ++a)
+      for (int b = a + 1; b < L; ++b) {
+        int ka = -1, kb = -1;
+        int64_t ga = 0, gb = 0;
+        for (int k = 0; k < I; ++k) {
+          if (nu[k] == a) {
+            const int64_t g = M[(size_t)k * L + b] - M[(size_t)k * L + a];
+            if (ka < 0 || g > ga) {
+              ga = g;
+              ka = k;
+            }
+          } else if (nu[k] == b) {
+            const int64_t g = M[(size_t)k * L + a] - M[(size_t)k * L + b];
+            if (kb < 0 || g > gb) {
+              gb = g;
+              kb = k;
+            }
+          }
+        }
+        if (ka >= 0 && kb >= 0 && ga + gb > 0) {
+          nu[ka] = b;
+          nu[kb] = a;
+          changed = true;
+        }
+      }
+  }
+  int64_t v = 0;
+  for (int k = 0; k < I; ++k) {
+    nu_out[k] = nu[k];
+    v += M[(size_t)k * L + nu[k]];
+  }
+  if (value) *value = v;
+}
+
 }  // namespace dtp

@@ -52,6 +52,12 @@ bool unrank_partition(int G, int L, int64_t rank, int32_t* h);
 // ---- exact balanced assignment (assign.cpp).  M is [I][L] row-major.
 // Returns the lexicographically smallest assignment maximising sum_k M[k][nu[k]].
 void balanced_assign_exact(int I, int L, const int64_t* M, int32_t* nu, int64_t* value);
+// The paper's approximate solver (dual ascent on device offsets, capacity fix-up, pairwise
+// swaps); balanced, never above the optimum, exact when L = 2.
+void balanced_assign_dual_ascent(int I, int L, const int64_t* M, int iterations, double decay,
+                                 int32_t* nu, int64_t* value);
+constexpr int kDualAscentIterations = 300;
+constexpr double kDualAscentDecay = 0.98;
 
 // ---- GPU partition scoring (scores.hip)
 struct ScoreWorkspace {

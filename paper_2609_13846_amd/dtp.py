@@ -40,7 +40,7 @@ class dtp_layer_desc(ctypes.Structure):
 class dtp_ca_options(ctypes.Structure):
     _fields_ = [("max_sweeps", ctypes.c_int32), ("freeze_heads", ctypes.c_int32),
                 ("freeze_neurons", ctypes.c_int32), ("minimise", ctypes.c_int32),
-                ("layer_mask", ctypes.c_void_p)]
+                ("layer_mask", ctypes.c_void_p), ("dual_ascent_neurons", ctypes.c_int32)]
 
 
 _P = ctypes.c_void_p
@@ -67,6 +67,8 @@ _SIGNATURES = {
     "dtp_encode_affinity": (_I32, [_P, _I64, _P]),
     "dtp_partition_scores": (_I32, [_I32, _I32, _I32, _P, _P, _P, _P, _I32, _P, ctypes.POINTER(_I64), _P]),
     "dtp_balanced_assign": (_I32, [_I32, _I32, _I32, _P, _P, _P, _P, _I32, _P, ctypes.POINTER(_I64)]),
+    "dtp_balanced_assign_dual_ascent": (_I32, [_I32, _I32, _I32, _P, _P, _P, _P, _I32, _P,
+                                               ctypes.POINTER(_I64)]),
     "dtp_coordinate_ascent": (_I32, [_I32, _I32, _I32, _I32, _P, _P, ctypes.POINTER(dtp_ca_options),
                                      _P, _P, ctypes.POINTER(_I64), ctypes.POINTER(ctypes.c_double),
                                      ctypes.POINTER(_I32), _P]),
@@ -217,25 +219,36 @@ def dtp_partition_scores(G, I, L, Q_up, nu, Q_down_prev=None, nu_prev=None, mini
     return best.value
 
 
-def dtp_balanced_assign(G, I, L, Q_up, h, Q_down=None, h_next=None, minimise=False):
-    """Host arrays in, (nu int32 [I], value) out."""
+def _assign(fn, G, I, L, Q_up, h, Q_down, h_next, minimise):
     qu = np.ascontiguousarray(Q_up, dtype=np.int64)
     hh = np.ascontiguousarray(h, dtype=np.int32)
     qd = None if Q_down is None else np.ascontiguousarray(Q_down, dtype=np.int64)
     hn = None if h_next is None else np.ascontiguousarray(h_next, dtype=np.int32)
     nu = np.zeros(max(I, 1), dtype=np.int32)
     val = _I64()
-    _check(lib().dtp_balanced_assign(G, I, L, _ptr(qu), _ptr(hh), _ptr(qd), _ptr(hn),
-                                     int(bool(minimise)), _ptr(nu), ctypes.byref(val)))
+    _check(fn(G, I, L, _ptr(qu), _ptr(hh), _ptr(qd), _ptr(hn), int(bool(minimise)), _ptr(nu),
+              ctypes.byref(val)))
     return nu[:I], val.value
 
 
+def dtp_balanced_assign(G, I, L, Q_up, h, Q_down=None, h_next=None, minimise=False):
+    """Host arrays in, (nu int32 [I], value) out."""
+    return _assign(lib().dtp_balanced_assign, G, I, L, Q_up, h, Q_down, h_next, minimise)
+
+
+def dtp_balanced_assign_dual_ascent(G, I, L, Q_up, h, Q_down=None, h_next=None, minimise=False):
+    """The paper's approximate neuron step: host arrays in, (nu int32 [I], value) out."""
+    return _assign(lib().dtp_balanced_assign_dual_ascent, G, I, L, Q_up, h, Q_down, h_next,
+                   minimise)
+
+
 def dtp_coordinate_ascent(N, G, I, L, A_up, A_down=None, max_sweeps=64, freeze_heads=False,
-                          freeze_neurons=False, minimise=False, layer_mask=None, stream=None):
+                          freeze_neurons=False, minimise=False, layer_mask=None, stream=None,
+                          dual_ascent_neurons=False):
     """A_up [N,G,I] (and A_down [N-1,I,G]) are device tensors; returns a dict of host results."""
     mask = None if layer_mask is None else np.ascontiguousarray(layer_mask, dtype=np.uint8)
     opt = dtp_ca_options(max_sweeps, int(freeze_heads), int(freeze_neurons), int(minimise),
-                         _ptr(mask))
+                         _ptr(mask), int(dual_ascent_neurons))
     h = np.zeros((N, G), dtype=np.int32)
     nu = np.zeros((N, I), dtype=np.int32)
     jf = _I64()

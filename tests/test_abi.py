@@ -84,19 +84,21 @@ def test_encode_arguments():
     assert lib.dtp_encode_affinity(a.ctypes.data, 0, q.ctypes.data) == dtp.DTP_ERR_INVALID_ARG
 
 
-def test_balanced_assign_arguments():
+@pytest.mark.parametrize("fn", ["dtp_balanced_assign", "dtp_balanced_assign_dual_ascent"])
+def test_balanced_assign_arguments(fn):
     Q = np.ones((8, 16), np.int64)
     h = np.arange(8) // 2
-    _expect(dtp.DTP_ERR_INVALID_ARG, dtp.dtp_balanced_assign, 8, 15, 4, Q, h)          # I % L
-    _expect(dtp.DTP_ERR_INVALID_ARG, dtp.dtp_balanced_assign, 8, 16, 3, Q, h)          # G % L
-    _expect(dtp.DTP_ERR_INVALID_ARG, dtp.dtp_balanced_assign, 8, 16, 4, Q, np.zeros(8))  # unbalanced
-    _expect(dtp.DTP_ERR_INVALID_ARG, dtp.dtp_balanced_assign, 8, 16, 4, Q, h + 4)      # not a device
-    _expect(dtp.DTP_ERR_UNSUPPORTED, dtp.dtp_balanced_assign, 16, 16, 16, np.ones((16, 16), np.int64),
+    assign = getattr(dtp, fn)
+    _expect(dtp.DTP_ERR_INVALID_ARG, assign, 8, 15, 4, Q, h)          # I % L
+    _expect(dtp.DTP_ERR_INVALID_ARG, assign, 8, 16, 3, Q, h)          # G % L
+    _expect(dtp.DTP_ERR_INVALID_ARG, assign, 8, 16, 4, Q, np.zeros(8))  # unbalanced
+    _expect(dtp.DTP_ERR_INVALID_ARG, assign, 8, 16, 4, Q, h + 4)      # not a device
+    _expect(dtp.DTP_ERR_UNSUPPORTED, assign, 16, 16, 16, np.ones((16, 16), np.int64),
             np.arange(16))                                                                  # L > 8
-    _expect(dtp.DTP_ERR_INVALID_ARG, dtp.dtp_balanced_assign, 8, 16, 4, Q, h, Q_down=Q.T.copy())
+    _expect(dtp.DTP_ERR_INVALID_ARG, assign, 8, 16, 4, Q, h, Q_down=Q.T.copy())
     lib = dtp.lib()
     v = ctypes.c_int64()
-    assert lib.dtp_balanced_assign(8, 16, 4, None, None, None, None, 0, None, ctypes.byref(v)) == \
+    assert getattr(lib, fn)(8, 16, 4, None, None, None, None, 0, None, ctypes.byref(v)) == \
         dtp.DTP_ERR_INVALID_ARG
 
 

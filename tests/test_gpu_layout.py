@@ -11,6 +11,7 @@ import pytest
 import torch
 
 from oracle import affinity as orc
+from oracle import dual_ascent as da
 from oracle import layout as lay
 from paper_2609_13846_amd import dtp, synth
 from tests import helpers as hp
@@ -94,6 +95,30 @@ def test_coordinate_ascent_modes_bit_exact():
         np.testing.assert_array_equal(res["h"], np.array(hs), err_msg=str(kw))
         np.testing.assert_array_equal(res["nu"], np.array(nus), err_msg=str(kw))
         assert res["J_fixed"] == J and res["sweeps"] == sweeps, kw
+
+
+@pytest.mark.parametrize("N,G,I,L,down", [(1, 8, 3072, 4, False), (3, 8, 1024, 4, True),
+                                          (2, 8, 3072, 2, True)])
+def test_coordinate_ascent_with_dual_ascent_neurons_bit_exact(N, G, I, L, down):
+    """The ascent with the paper's approximate neuron step, against the oracle ascent with
+    the oracle of that step; with L = 2 it also equals the exact ascent."""
+    announce(f"coordinate ascent, dual-ascent neurons N={N} G={G} I={I} L={L} down={down}")
+    rng = np.random.default_rng(N * 31 + L)
+    Au = rand_A(rng, (N, G, I))
+    Ad = rand_A(rng, (N - 1, I, G)) if down else None
+    res = dtp.dtp_coordinate_ascent(N, G, I, L, torch.from_numpy(Au).cuda(),
+                                    None if Ad is None else torch.from_numpy(Ad).cuda(),
+                                    dual_ascent_neurons=True)
+    Qu = [lay.encode(Au[i]) for i in range(N)]
+    Qd = [lay.encode(Ad[i]) for i in range(N - 1)] if down else None
+    step = lambda M, minimise: da.assign(-M if minimise else M)[0]
+    hs, nus, J, sweeps = lay.coordinate_ascent(Qu, Qd, L, neuron_step=step)
+    np.testing.assert_array_equal(res["h"], np.array(hs))
+    np.testing.assert_array_equal(res["nu"], np.array(nus))
+    assert res["J_fixed"] == J and res["sweeps"] == sweeps
+    exact = lay.coordinate_ascent(Qu, Qd, L)
+    if L == 2:
+        assert J == exact[2]
 
 
 def test_layout_from_gpu_affinity_matches_oracle_objective():

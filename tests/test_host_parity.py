@@ -4,6 +4,7 @@ the host by design; no GPU is involved)."""
 import numpy as np
 import pytest
 
+from oracle import dual_ascent as da
 from oracle import layout as lay
 from paper_2609_13846_amd import dtp
 
@@ -79,6 +80,39 @@ def test_balanced_assign_ties_bit_exact(I, L):
     Z = np.zeros((G, I), np.int64)
     nu, v = dtp.dtp_balanced_assign(G, I, L, Z, np.arange(G) // (G // L))
     np.testing.assert_array_equal(nu, np.arange(I) // (I // L))
+
+
+@pytest.mark.parametrize("G,I,L,down,minimise", CASES)
+def test_dual_ascent_assign_bit_exact(G, I, L, down, minimise):
+    """The paper's approximate neuron step, library against oracle, bit for bit."""
+    rng = np.random.default_rng(G * 1000 + I + L + 7)
+    Qu = lay.encode(rand_A(rng, (G, I)))
+    Qd = lay.encode(rand_A(rng, (I, G))) if down else None
+    h = rng.permutation(np.arange(G) // (G // L))
+    hn = rng.permutation(np.arange(G) // (G // L)) if down else None
+    nu, v = dtp.dtp_balanced_assign_dual_ascent(G, I, L, Qu, h, Qd, hn, minimise)
+    M = lay.neuron_gain(Qu, h, L, Qd, hn)
+    onu, ov = da.assign(-M if minimise else M)
+    np.testing.assert_array_equal(nu, onu)
+    assert v == (-ov if minimise else ov)
+    assert v == int(M[np.arange(I), onu].sum())
+    _, vopt = lay.balanced_assign(M, minimise)
+    assert (v >= vopt) if minimise else (v <= vopt)
+    if L == 2:
+        assert v == vopt
+
+
+@pytest.mark.parametrize("I,L", [(12, 4), (64, 4), (40, 2), (48, 8)])
+def test_dual_ascent_ties_bit_exact(I, L):
+    rng = np.random.default_rng(I * L + 1)
+    G = 8
+    for trial in range(4):
+        Qu = rng.integers(0, 3, size=(G, I)).astype(np.int64) << 40   # many equal gains
+        h = rng.permutation(np.arange(G) // (G // L))
+        nu, v = dtp.dtp_balanced_assign_dual_ascent(G, I, L, Qu, h)
+        onu, ov = da.assign(lay.neuron_gain(Qu, h, L))
+        assert v == ov
+        np.testing.assert_array_equal(nu, onu)
 
 
 # ----------------------------------------------------------------------------- random layouts
