@@ -169,3 +169,35 @@ def test_add_score_power_of_two_head_scale_is_exact():
     A2 = hp.gpu_affinity(wl, w, x, a2, score="add")
     np.testing.assert_array_equal(A2[g], 4.0 * A1[g])
     np.testing.assert_array_equal(np.delete(A2, g, axis=0), np.delete(A1, g, axis=0))
+
+
+@pytest.mark.parametrize("name", ["danube3-500m", "8b-class-4layer"])
+def test_affinity_full_workload_sampled_neurons(name):
+    """The whole calibration set of one layer (131,072 tokens, streamed in the workload's
+    16,384-token chunks as the full-model run does), generated on the device; the oracle
+    recomputes 32 sampled neurons chunk by chunk from the same bytes (token sums add)."""
+    import torch
+    wl = synth.WORKLOADS[name]
+    dev = torch.device("cuda", 0)
+    announce(f"affinity {name} T={wl.tokens} in chunks of {wl.chunk} (full, device data)")
+    w = synth.device_weights(wl, 0, dev)
+    layer = hp.layer_for(wl)
+    A = torch.zeros(wl.n_kv_groups, wl.n_neurons, dtype=torch.float32, device=dev)
+    rng = np.random.default_rng(1)
+    cols = np.sort(np.concatenate([rng.choice(wl.n_neurons, 28, replace=False),
+                                   [0, 63, 64, wl.n_neurons - 1]]))
+    f = lambda t: t.float().cpu().numpy().astype(np.float64)
+    wh = {k: f(w[k]) for k in ("w_o", "gamma", "w_gate", "w_up", "w_down")}
+    ref = np.zeros((wl.n_kv_groups, len(cols)))
+    try:
+        dtp.dtp_layer_set_weights(layer, w["w_o"], w["gamma"], w["w_gate"], w["w_up"], w["w_down"])
+        for c in range(wl.tokens // wl.chunk):
+            x, a = synth.device_tokens(wl, 0, w, wl.chunk, c, dev)
+            dtp.dtp_affinity_accumulate(layer, x, a, wl.chunk, A)
+            ref += orc.affinity_folded(f(x), f(a).reshape(wl.chunk, wl.n_q_heads, wl.head_dim),
+                                       wh["w_o"], wh["gamma"], wh["w_gate"], wh["w_up"],
+                                       wh["w_down"], wl.n_kv_groups, wl.rms_eps, neurons=cols)
+        torch.cuda.synchronize()
+        hp.assert_affinity_close(A.cpu().numpy()[:, cols], ref)
+    finally:
+        dtp.dtp_layer_destroy(layer)
