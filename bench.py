@@ -45,14 +45,15 @@ def kernel_hash() -> str:
 
 
 def traffic_record(wl):
-    """HBM bytes per launch from the committed PMC summary, if it matches this kernel."""
+    """The committed PMC summary of the affinity kernel (HBM bytes, MFMA busy fraction and
+    clock per launch), if it was taken on this kernel source and workload; else {}."""
     try:
         rec = json.load(open(TRAFFIC_FILE))
     except (OSError, ValueError):
-        return None
+        return {}
     if rec.get("kernel_sha") != kernel_hash() or rec.get("workload") != wl.name:
-        return None
-    return rec.get("bytes_per_launch")
+        return {}
+    return rec
 
 
 def make_layer(dtp, synth, wl, layer_idx, device):
@@ -61,6 +62,31 @@ def make_layer(dtp, synth, wl, layer_idx, device):
                                  wl.head_dim, wl.rms_eps,
                                  dtp.DTP_BF16 if wl.dtype == "bf16" else dtp.DTP_F32)
     return layer, w
+
+
+def library_gemm(torch, device, wl, tokens):
+    """A plain bf16 torch.matmul (the vendor GEMM library) with the FLOPs of one affinity
+    launch: [tokens x (d + H*dh)] @ [(d + H*dh) x 2I], no epilogue.  Context for the fused
+    kernel's fraction of peak: what a library GEMM of the same size reaches on this GPU."""
+    K = wl.d_model + wl.n_q_heads * wl.head_dim
+    gen = torch.Generator(device=device).manual_seed(0)
+    a = torch.randn(tokens, K, device=device, dtype=torch.bfloat16, generator=gen)
+    b = torch.randn(K, 2 * wl.n_neurons, device=device, dtype=torch.bfloat16, generator=gen) * 0.02
+    for _ in range(3):
+        c = a @ b
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    reps = 10
+    e0.record()
+    for _ in range(reps):
+        c = a @ b
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / reps
+    tflops = 2.0 * tokens * K * 2 * wl.n_neurons / (ms * 1e-3) / 1e12
+    del a, b, c
+    return {"what": f"torch.matmul bf16 [{tokens} x {K}] @ [{K} x {2 * wl.n_neurons}], no epilogue",
+            "ms": ms, "tflops": tflops, "frac": tflops / PEAK_BF16_TFLOPS}
 
 
 def cpu_baseline(wl, x, attn, w, L, n_tokens):
@@ -154,6 +180,8 @@ def main():
     ap.add_argument("--workload", default="qwen3-0.6b-layer")
     ap.add_argument("--cpu-sample-tokens", type=int, default=49152)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-library-gemm", action="store_true",
+                    help="skip the library GEMM of the same FLOPs (context, untimed)")
     ap.add_argument("--full-model", nargs="*", default=None, metavar="WORKLOAD",
                     help="also time the full-model layout (default workloads: "
                          "qwen3-0.6b-model danube3-500m 8b-class-4layer)")
@@ -239,7 +267,7 @@ def main():
     f_launch = flops_per_token(wl) * T / max(launches_per_step, 1)
     avg_ms = kern_ms / max(launches, 1)
     achieved = f_launch / (avg_ms * 1e-3) / 1e12
-    traffic = traffic_record(wl)
+    pmc = traffic_record(wl)
     out = {
         "metric": METRIC,
         "value": value,
@@ -258,7 +286,10 @@ def main():
                    "shards": L, "parallelism": "single GPU; shards are logical"},
         "roofline": {"bound": "mfma", "kernel": "affinity_bf16_kernel",
                      "achieved": achieved, "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
-                     "frac": achieved / PEAK_BF16_TFLOPS, "traffic": traffic,
+                     "frac": achieved / PEAK_BF16_TFLOPS, "traffic": pmc.get("bytes_per_launch"),
+                     "traffic_gbs": (pmc["bytes_per_launch"] / (avg_ms * 1e-3) / 1e9
+                                     if pmc.get("bytes_per_launch") else None),
+                     "mfma_busy_pmc": pmc.get("mfma_busy"), "clock_ghz_pmc": pmc.get("clock_ghz"),
                      "avg_launch_ms": avg_ms, "launches": launches,
                      "tokens_per_launch": T / max(launches_per_step, 1),
                      "flops_per_launch": f_launch},
@@ -268,6 +299,9 @@ def main():
         "layout": {"J": res["J"], "sweeps": res["sweeps"], "neuron_step": neuron_steps},
         "context": "paper: 65,536-token affinity pass of a 28-layer model in 51 s on one RTX 5090",
     }
+    if not args.no_library_gemm:
+        out["roofline"]["library_gemm_same_flops"] = library_gemm(
+            torch, device, wl, int(T / max(launches_per_step, 1)))
     if not args.no_cpu_baseline:
         log(f"cpu baseline: oracle on {args.cpu_sample_tokens} tokens")
         out["cpu_baseline"] = cpu_baseline(wl, x, attn, w, L, args.cpu_sample_tokens)

@@ -3,13 +3,18 @@
     python -m paper_2609_13846_amd.rocprof collect --out gpurun_out/prof
     python -m paper_2609_13846_amd.rocprof summarize --dir gpurun_out/prof --profiles profiles
 
-``collect`` runs five rocprofv3 passes of ``bench.py``, each in its own process with its
+``collect`` runs six rocprofv3 passes of ``bench.py``, each in its own process with its
 own time limit, writing CSV output (no database files):
 
 * ``trace``: ``--kernel-trace --stats`` of a timed bench run;
 * ``fetch`` / ``write``: ``--pmc FETCH_SIZE`` and ``--pmc WRITE_SIZE`` of a short run;
 * ``copyf`` / ``copyw``: the same counters on a plain 1 GiB device copy, which fixes the
-  scale of each counter on this GPU (bytes the copy moves / bytes the counter reports).
+  scale of each counter on this GPU (bytes the copy moves / bytes the counter reports);
+* ``mfma``: ``--kernel-trace`` with the SQ and GRBM counters of MFMA and VALU work:
+  SQ_VALU_MFMA_BUSY_CYCLES sums the matrix-core cycles of every SIMD (16 per
+  ``v_mfma_f32_16x16x32_bf16``, 32 per ``32x32x16``), GRBM_GUI_ACTIVE the GPU cycles of each
+  of the 8 XCDs, so the MFMA busy fraction is MFMA_BUSY / (GRBM_GUI_ACTIVE / 8 * 1024 SIMDs)
+  and GRBM_GUI_ACTIVE / 8 over the launch's duration is the clock it ran at.
 
 ``summarize`` writes a markdown summary of the kernel trace and the traffic of the
 affinity kernel (bytes per launch, counter scales applied) to ``profiles/``, plus the
@@ -30,6 +35,11 @@ import sys
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 KERNEL_SRC = os.path.join(ROOT, "paper_2609_13846_amd", "csrc", "affinity.hip")
 COPY_MIB = 1024
+MFMA_COUNTERS = ["SQ_VALU_MFMA_BUSY_CYCLES", "SQ_BUSY_CYCLES", "SQ_INSTS_MFMA", "SQ_INSTS_VALU",
+                 "SQ_INSTS_LDS", "SQ_LDS_BANK_CONFLICT", "SQ_LDS_IDX_ACTIVE", "SQ_WAVE_CYCLES",
+                 "GRBM_GUI_ACTIVE"]
+N_XCD = 8
+N_SIMD = 1024
 
 
 def kernel_sha() -> str:
@@ -38,8 +48,8 @@ def kernel_sha() -> str:
 
 def _passes(out: str, steps: int):
     bench = [sys.executable, os.path.join(ROOT, "bench.py")]
-    timed = bench + ["--steps", str(steps), "--warmup", "2", "--no-cpu-baseline"]
-    short = bench + ["--steps", "2", "--warmup", "1", "--no-cpu-baseline"]
+    timed = bench + ["--steps", str(steps), "--warmup", "2", "--no-cpu-baseline", "--no-library-gemm"]
+    short = bench + ["--steps", "2", "--warmup", "1", "--no-cpu-baseline", "--no-library-gemm"]
     copy = bench + ["--copy-calibration", str(COPY_MIB)]
     return [
         ("trace", ["--kernel-trace", "--stats"], timed, 300),
@@ -47,6 +57,7 @@ def _passes(out: str, steps: int):
         ("write", ["--pmc", "WRITE_SIZE"], short, 180),
         ("copyf", ["--pmc", "FETCH_SIZE"], copy, 120),
         ("copyw", ["--pmc", "WRITE_SIZE"], copy, 120),
+        ("mfma", ["--kernel-trace", "--pmc", *MFMA_COUNTERS], short, 180),
     ]
 
 
@@ -88,6 +99,19 @@ def _counter(dirname, kernel_sub):
     return vals
 
 
+def _counters(dirname, kernel_sub):
+    """{counter: mean per dispatch} over the dispatches of kernels matching kernel_sub, and
+    the mean duration (ns) of those dispatches from the pass's kernel trace."""
+    acc = {}
+    for row in csv.DictReader(open(_one(os.path.join(dirname, "**", "*counter_collection.csv")))):
+        if kernel_sub in row["Kernel_Name"]:
+            acc.setdefault(row["Counter_Name"], []).append(float(row["Counter_Value"]))
+    durs = [int(r["End_Timestamp"]) - int(r["Start_Timestamp"])
+            for r in csv.DictReader(open(_one(os.path.join(dirname, "**", "*kernel_trace.csv"))))
+            if kernel_sub in r["Kernel_Name"]]
+    return {k: sum(v) / len(v) for k, v in acc.items()}, (sum(durs) / len(durs) if durs else 0.0)
+
+
 def summarize(d: str, profiles: str, workload: str, bench_cmd: str) -> None:
     stats = list(csv.DictReader(open(_one(os.path.join(d, "trace", "**", "*kernel_stats.csv")))))
     stats.sort(key=lambda r: -float(r["TotalDurationNs"]))
@@ -127,11 +151,34 @@ def summarize(d: str, profiles: str, workload: str, bench_cmd: str) -> None:
               f"- FETCH_SIZE: {sum(fk) / len(fk):.0f} KiB per launch raw, {fetch_b / 1e9:.3f} GB scaled",
               f"- WRITE_SIZE: {sum(wk) / len(wk):.0f} KiB per launch raw, {write_b / 1e9:.3f} GB scaled",
               f"- total: {(fetch_b + write_b) / 1e9:.3f} GB per launch ({len(fk)} launches sampled)"]
+    if aff:
+        gbs = (fetch_b + write_b) / (float(aff[0]["AverageNs"]) * 1e-9) / 1e9
+        lines += [f"- at the traced average duration: {gbs:.0f} GB/s, {gbs / 8000:.1%} of the 8 TB/s HBM peak"]
+    mdir = os.path.join(d, "mfma")
+    if os.path.isdir(mdir):
+        m, dur_ns = _counters(mdir, "affinity_bf16_kernel")
+        cyc = m["GRBM_GUI_ACTIVE"] / N_XCD
+        busy = m["SQ_VALU_MFMA_BUSY_CYCLES"] / (cyc * N_SIMD)
+        clock = cyc / dur_ns if dur_ns else 0.0
+        lines += ["", "## MFMA and VALU work of the affinity kernel (--pmc, one pass)", "",
+                  f"Counters: {', '.join(MFMA_COUNTERS)}; means per dispatch.", "",
+                  f"- MFMA busy: {busy:.1%} of the SIMD cycles "
+                  f"(SQ_VALU_MFMA_BUSY_CYCLES {m['SQ_VALU_MFMA_BUSY_CYCLES']:.4g} / "
+                  f"(GRBM_GUI_ACTIVE / {N_XCD} = {cyc:.4g} cycles x {N_SIMD} SIMDs))",
+                  f"- clock during the launch: {clock:.2f} GHz (GRBM_GUI_ACTIVE / {N_XCD} over "
+                  f"{dur_ns / 1e3:.0f} us)",
+                  f"- MFMA instructions: {m['SQ_INSTS_MFMA']:.4g} per launch; VALU instructions "
+                  f"{m['SQ_INSTS_VALU']:.4g}; LDS instructions {m['SQ_INSTS_LDS']:.4g}",
+                  f"- LDS bank conflicts: {m['SQ_LDS_BANK_CONFLICT'] / max(m['SQ_LDS_IDX_ACTIVE'], 1):.1%} "
+                  f"of the LDS active cycles"]
     open(os.path.join(profiles, name + ".md"), "w").write("\n".join(lines) + "\n")
+    mf = {}
+    if os.path.isdir(mdir):
+        mf = {"mfma_busy": busy, "clock_ghz": clock, "mfma_insts_per_launch": m["SQ_INSTS_MFMA"]}
     rec = {"kernel": "affinity_bf16_kernel", "workload": workload, "kernel_sha": kernel_sha(),
            "fetch_bytes_per_launch": fetch_b, "write_bytes_per_launch": write_b,
            "bytes_per_launch": fetch_b + write_b, "fetch_scale": f_scale, "write_scale": w_scale,
-           "avg_launch_us": float(aff[0]["AverageNs"]) / 1e3 if aff else None}
+           "avg_launch_us": float(aff[0]["AverageNs"]) / 1e3 if aff else None, **mf}
     json.dump(rec, open(os.path.join(profiles, "affinity_traffic.json"), "w"), indent=1)
     print(f"wrote {os.path.join(profiles, name + '.md')} and affinity_traffic.json")
 
