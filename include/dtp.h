@@ -163,6 +163,13 @@ dtp_status dtp_partition_unrank(int32_t G, int32_t L, int64_t rank, int32_t* h);
  * DTP_ERR_DEGENERATE if any entry is negative or non-finite, or all are zero. */
 dtp_status dtp_encode_affinity(const float* A, int64_t n, int64_t* Q);
 
+/* The same codes computed on the GPU (the coordinate ascent encodes its matrices this way).
+ *   A dev [n] fp32 raw affinity, 1 <= n <= 2^30; Q dev [n] int64 output (caller-owned).
+ * Enqueued on `stream`, which is then synchronised to read the outcome: DTP_ERR_DEGENERATE
+ * (Q unspecified) if an entry is negative or non-finite, or all are zero; else the codes
+ * equal dtp_encode_affinity's bit for bit.  Uses a few bytes of stream-ordered scratch. */
+dtp_status dtp_encode_affinity_device(const float* A, int64_t n, int64_t* Q, void* stream);
+
 /* Head step of one layer i (Section 3, "Optimiser"): score every labelled balanced
  * partition h of the G KV groups,
  *   score(h) = sum_g C[g, h(g)],

@@ -188,6 +188,23 @@ dtp_status dtp_encode_affinity(const float* A, int64_t n, int64_t* Q) {
   return encode_unit_mass(A, n, Q);
 }
 
+dtp_status dtp_encode_affinity_device(const float* A, int64_t n, int64_t* Q, void* stream) {
+  clear_error();
+  DTP_CHECK(A != nullptr && Q != nullptr, DTP_ERR_INVALID_ARG, "A or Q is NULL");
+  DTP_CHECK(n >= 1 && n <= (int64_t(1) << 30), DTP_ERR_INVALID_ARG,
+            "n=%lld outside [1, 2^30]", (long long)n);
+  hipStream_t s = (hipStream_t)stream;
+  DevBuf stats_dev(s);
+  DTP_HIP(stream_alloc(&stats_dev.p, sizeof(EncodeStats), s));
+  dtp_status st = launch_encode_unit_mass(A, 1, nullptr, 0, n, Q, nullptr,
+                                          (EncodeStats*)stats_dev.p, s);
+  if (st != DTP_OK) return st;
+  EncodeStats stats;
+  DTP_HIP(hipMemcpyAsync(&stats, stats_dev.p, sizeof(EncodeStats), hipMemcpyDeviceToHost, s));
+  DTP_HIP(hipStreamSynchronize(s));
+  return check_encode_stats(stats, "matrix", 0);
+}
+
 dtp_status dtp_balanced_assign(int32_t G, int32_t I, int32_t L, const int64_t* Q_up,
                                const int32_t* h, const int64_t* Q_down, const int32_t* h_next,
                                int32_t minimise, int32_t* nu, int64_t* value) {
@@ -308,23 +325,33 @@ dtp_status dtp_coordinate_ascent(int32_t N, int32_t G, int32_t I, int32_t L, con
   const bool has_down = A_down != nullptr;
   const size_t nup = (size_t)N * G * I, ndown = has_down ? (size_t)(N - 1) * I * G : 0;
 
-  // Raw affinity to the host, one unit-mass code per matrix.
-  std::vector<float> Au(nup), Ad(ndown);
-  DTP_HIP(hipMemcpyAsync(Au.data(), A_up, sizeof(float) * nup, hipMemcpyDeviceToHost, s));
-  if (has_down)
-    DTP_HIP(hipMemcpyAsync(Ad.data(), A_down, sizeof(float) * ndown, hipMemcpyDeviceToHost, s));
-  DTP_HIP(hipStreamSynchronize(s));
+  // Unit-mass codes of every matrix, computed on the device where the head step reads
+  // them; the host copy feeds the neuron step and J.  Layout of the scratch block:
+  // [encode stats | Q_up | Q_down | nu].
+  const int nmat = N + (has_down ? N - 1 : 0);
+  const size_t st_bytes = sizeof(EncodeStats) * nmat;
+  const size_t qu_bytes = sizeof(int64_t) * nup, qd_bytes = sizeof(int64_t) * ndown;
+  DevBuf block(s);
+  DTP_HIP(stream_alloc(&block.p, st_bytes + qu_bytes + qd_bytes + sizeof(int32_t) * (size_t)N * I, s));
+  EncodeStats* st_dev = (EncodeStats*)block.p;
+  int64_t* qu_dev = (int64_t*)((char*)block.p + st_bytes);
+  int64_t* qd_dev = has_down ? qu_dev + nup : nullptr;
+  int32_t* nu_dev = (int32_t*)((char*)qu_dev + qu_bytes + qd_bytes);
+  st = launch_encode_unit_mass(A_up, N, A_down, has_down ? N - 1 : 0, (int64_t)G * I, qu_dev,
+                               qd_dev, st_dev, s);
+  if (st != DTP_OK) return st;
+  std::vector<EncodeStats> stats(nmat);
   std::vector<int64_t> Qu(nup), Qd(ndown);
-  for (int i = 0; i < N; ++i) {
-    st = encode_unit_mass(Au.data() + (size_t)i * G * I, (int64_t)G * I, Qu.data() + (size_t)i * G * I);
-    if (st != DTP_OK) return fail(st, "layer %d up affinity: %s", i, dtp_last_error());
-    if (has_down && i + 1 < N) {
-      st = encode_unit_mass(Ad.data() + (size_t)i * I * G, (int64_t)I * G, Qd.data() + (size_t)i * I * G);
-      if (st != DTP_OK) return fail(st, "layer %d down affinity: %s", i, dtp_last_error());
-    }
+  DTP_HIP(hipMemcpyAsync(stats.data(), st_dev, st_bytes, hipMemcpyDeviceToHost, s));
+  DTP_HIP(hipMemcpyAsync(Qu.data(), qu_dev, qu_bytes, hipMemcpyDeviceToHost, s));
+  if (has_down) DTP_HIP(hipMemcpyAsync(Qd.data(), qd_dev, qd_bytes, hipMemcpyDeviceToHost, s));
+  DTP_HIP(hipStreamSynchronize(s));
+  for (int m = 0; m < nmat; ++m) {
+    st = m < N ? check_encode_stats(stats[m], "up affinity of layer", m)
+               : check_encode_stats(stats[m], "down affinity of layer", m - N);
+    if (st != DTP_OK) return st;
   }
 
-  // Device copies of the codes for the head step.
   ScoreWorkspace ws;
   st = score_workspace_create(&ws, N, G, I, L, s);
   if (st != DTP_OK) {
@@ -335,16 +362,7 @@ dtp_status dtp_coordinate_ascent(int32_t N, int32_t G, int32_t I, int32_t L, con
     ScoreWorkspace* w;
     ~WsGuard() { score_workspace_destroy(w); }
   } guard{&ws};
-  // One device block for the codes and the neuron assignments: [Q_up | Q_down | nu].
-  DevBuf block(s);
-  const size_t qu_bytes = sizeof(int64_t) * nup, qd_bytes = sizeof(int64_t) * ndown;
-  DTP_HIP(stream_alloc(&block.p, qu_bytes + qd_bytes + sizeof(int32_t) * (size_t)N * I, s));
-  int64_t* qu_dev = (int64_t*)block.p;
-  int64_t* qd_dev = has_down ? qu_dev + nup : nullptr;
-  int32_t* nu_dev = (int32_t*)((char*)block.p + qu_bytes + qd_bytes);
-  DTP_HIP(hipMemcpyAsync(qu_dev, Qu.data(), qu_bytes, hipMemcpyHostToDevice, s));
-  if (has_down) DTP_HIP(hipMemcpyAsync(qd_dev, Qd.data(), qd_bytes, hipMemcpyHostToDevice, s));
-  const std::vector<uint8_t> table = enumerate_partitions(G, L);
+  const std::vector<uint8_t>& table = ws.host_table;
 
   // Contiguous start.
   std::vector<int32_t> hs((size_t)N * G), nus((size_t)N * I);

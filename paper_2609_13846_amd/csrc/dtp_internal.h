@@ -44,6 +44,21 @@ hipError_t stream_free(void* p, hipStream_t s);
 // ---- unit-mass fixed point (encode.cpp)
 dtp_status encode_unit_mass(const float* A, int64_t n, int64_t* Q);
 
+// ---- the same codes on the GPU (encode_device.hip), for n_up + n_down matrices of n
+// entries: matrix m < n_up reads A_up + m n and writes Q_up + m n, the others A_down and
+// Q_down.  Enqueues on `s`; stats (device, one per matrix) says, once the stream has run,
+// whether each matrix was encodable (check_encode_stats on a host copy); the codes of a
+// matrix that was not are left unwritten.
+struct EncodeStats {
+  unsigned long long maxbits;  // fp32 bits of the largest entry
+  unsigned long long badidx;   // smallest index of a negative or non-finite entry, or ~0
+  unsigned long long s_lo, s_hi;  // sum of the q codes, 128-bit
+};
+dtp_status launch_encode_unit_mass(const float* A_up, int n_up, const float* A_down, int n_down,
+                                   int64_t n, int64_t* Q_up, int64_t* Q_down, EncodeStats* stats,
+                                   hipStream_t s);
+dtp_status check_encode_stats(const EncodeStats& st, const char* what, int index);
+
 // ---- labelled balanced partitions (partitions.cpp)
 int64_t count_partitions(int G, int L);               // -1 if invalid or > 2^62
 std::vector<uint8_t> enumerate_partitions(int G, int L);  // [P][G], lexicographic

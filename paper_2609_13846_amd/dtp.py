@@ -65,6 +65,7 @@ _SIGNATURES = {
     "dtp_partition_count": (_I64, [_I32, _I32]),
     "dtp_partition_unrank": (_I32, [_I32, _I32, _I64, _P]),
     "dtp_encode_affinity": (_I32, [_P, _I64, _P]),
+    "dtp_encode_affinity_device": (_I32, [_P, _I64, _P, _P]),
     "dtp_partition_scores": (_I32, [_I32, _I32, _I32, _P, _P, _P, _P, _I32, _P, ctypes.POINTER(_I64), _P]),
     "dtp_balanced_assign": (_I32, [_I32, _I32, _I32, _P, _P, _P, _P, _I32, _P, ctypes.POINTER(_I64)]),
     "dtp_balanced_assign_dual_ascent": (_I32, [_I32, _I32, _I32, _P, _P, _P, _P, _I32, _P,
@@ -207,6 +208,12 @@ def dtp_encode_affinity(A):
     q = np.zeros(a.shape, dtype=np.int64)
     _check(lib().dtp_encode_affinity(_ptr(a), a.size, _ptr(q)))
     return q
+
+
+def dtp_encode_affinity_device(A, Q, stream=None):
+    """A (fp32) and Q (int64, same number of elements) are device tensors; Q is written."""
+    _check(lib().dtp_encode_affinity_device(_ptr(A), A.numel(), _ptr(Q), _stream(stream)))
+    return Q
 
 
 def dtp_partition_scores(G, I, L, Q_up, nu, Q_down_prev=None, nu_prev=None, minimise=False,

@@ -102,6 +102,14 @@ def test_balanced_assign_arguments(fn):
         dtp.DTP_ERR_INVALID_ARG
 
 
+def test_device_encode_arguments_checked_before_gpu():
+    lib = dtp.lib()
+    assert lib.dtp_encode_affinity_device(None, 5, 1, None) == dtp.DTP_ERR_INVALID_ARG
+    assert lib.dtp_encode_affinity_device(1, 5, None, None) == dtp.DTP_ERR_INVALID_ARG
+    assert lib.dtp_encode_affinity_device(1, 0, 1, None) == dtp.DTP_ERR_INVALID_ARG
+    assert lib.dtp_encode_affinity_device(1, (1 << 30) + 1, 1, None) == dtp.DTP_ERR_INVALID_ARG
+
+
 def test_partition_scores_and_ascent_arguments_checked_before_gpu():
     lib = dtp.lib()
     best = ctypes.c_int64()
