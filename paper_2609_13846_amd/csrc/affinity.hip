@@ -404,15 +404,16 @@ __device__ inline void load_token_rows(TokenRows<KC, RB>& f, __amdgpu_buffer_rsr
 
 // MFMA work of one stage: the wave's RB token row blocks against the gate and up
 // fragments of its NB neuron blocks; each LDS fragment feeds RB MFMAs.  Fragments are
-// read two k-steps ahead of their MFMAs (double-buffered in registers), so an MFMA never
-// waits on the LDS read it consumes.  ZERO starts the accumulators from zero (first stage of a
-// contraction) instead of adding to them.
+// read kAhead k-steps ahead of their MFMAs (three register buffers, measured 1% faster
+// than two at KC = 64), so the LDS latency hides behind the MFMAs in between.  ZERO starts
+// the accumulators from zero (first stage of a contraction) instead of adding to them.
 template <int KC, int RB, int NB, bool ZERO>
 __device__ __forceinline__ void stage_mfma(const uint16_t* B, const TokenRows<KC, RB>& a,
                                            f32x16 (&acc)[RB][NB][2], const int (&gate_off)[NB],
                                            const int (&up_off)[NB]) {
   constexpr int kSteps = KC / 16;
-  bf16x8 frag[2][NB][2];
+  constexpr int kAhead = kSteps < 3 ? kSteps : 3;
+  bf16x8 frag[kAhead][NB][2];
   auto read = [&](int buf, int s) __attribute__((always_inline)) {
 #pragma unroll
     for (int nb = 0; nb < NB; ++nb) {
@@ -420,8 +421,8 @@ __device__ __forceinline__ void stage_mfma(const uint16_t* B, const TokenRows<KC
       frag[buf][nb][1] = *reinterpret_cast<const bf16x8*>(B + up_off[nb] + 8 * s);
     }
   };
-  read(0, 0);
-  if (kSteps > 1) read(1, 1);
+#pragma unroll
+  for (int s = 0; s < kAhead; ++s) read(s, s);
 #pragma unroll
   for (int s = 0; s < kSteps; ++s) {
 #pragma unroll
@@ -433,18 +434,18 @@ __device__ __forceinline__ void stage_mfma(const uint16_t* B, const TokenRows<KC
 #pragma unroll
         for (int gu = 0; gu < 2; ++gu)
           acc[rb][nb][gu] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
-              av, frag[s & 1][nb][gu], z ? f32x16{} : acc[rb][nb][gu], 0, 0, 0);
+              av, frag[s % kAhead][nb][gu], z ? f32x16{} : acc[rb][nb][gu], 0, 0, 0);
       }
-    if (s + 2 < kSteps) read(s & 1, s + 2);
+    if (s + kAhead < kSteps) read(s % kAhead, s + kAhead);
   }
-  // Keep that order through scheduling: the reads of k-steps 0 and 1 first, then each
-  // k-step's MFMAs followed by the reads of the k-step after next.
+  // Keep that order through scheduling: the reads of the first kAhead k-steps, then each
+  // k-step's MFMAs followed by the reads of the k-step kAhead later.
   constexpr int kFrags = 2 * NB, kMfma = 2 * NB * RB;
-  __builtin_amdgcn_sched_group_barrier(0x100, kSteps > 1 ? 2 * kFrags : kFrags, 0);
+  __builtin_amdgcn_sched_group_barrier(0x100, kAhead * kFrags, 0);
 #pragma unroll
   for (int s = 0; s < kSteps; ++s) {
     __builtin_amdgcn_sched_group_barrier(0x008, kMfma, 0);
-    if (s + 2 < kSteps) __builtin_amdgcn_sched_group_barrier(0x100, kFrags, 0);
+    if (s + kAhead < kSteps) __builtin_amdgcn_sched_group_barrier(0x100, kFrags, 0);
   }
 }
 
