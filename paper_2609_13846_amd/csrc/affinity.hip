@@ -476,8 +476,10 @@ template <int RB, int NB>
 struct Coefs<RB, NB, true> {
   uint32_t v[RB][NB][16];  // c1 in the low half, c2 in the high half
   __device__ __forceinline__ void set(int rb, int nb, int i, float a, float b) {
-    v[rb][nb][i] = (uint32_t)__builtin_bit_cast(uint16_t, (_Float16)a) |
-                   ((uint32_t)__builtin_bit_cast(uint16_t, (_Float16)b) << 16);
+    half2_t c;
+    c.x = (_Float16)a;
+    c.y = (_Float16)b;
+    v[rb][nb][i] = __builtin_bit_cast(uint32_t, c);
   }
   __device__ __forceinline__ float c1(int rb, int nb, int i) const {
     return (float)__builtin_bit_cast(_Float16, (uint16_t)(v[rb][nb][i] & 0xffffu));
@@ -644,10 +646,13 @@ affinity_bf16_kernel(AffinityArgs p) {
                 const float g = acc[rb][nb][0][i] * ri;
                 const float u = acc[rb][nb][1][i] * ri;
                 const float sg = __builtin_amdgcn_rcpf(1.0f + __expf(-g));
-                if (ADD)
+                if (ADD) {
                   cf.set(rb, nb, i, rs, rs);
-                else
-                  cf.set(rb, nb, i, sg * (1.0f + g * (1.0f - sg)) * u * rs, g * sg * rs);
+                } else {
+                  // silu(g) = g sg, silu'(g) = sg + silu(g) (1 - sg)
+                  const float sl = g * sg;
+                  cf.set(rb, nb, i, (fmaf(-sl, sg, sl) + sg) * u * rs, sl * rs);
+                }
               }
             }
           }
