@@ -449,6 +449,74 @@ __device__ __forceinline__ void stage_mfma(const uint16_t* B, const TokenRows<KC
   }
 }
 
+// Weight stages of KC = 64 copied into LDS by the buffer unit (buffer_load ... lds), no
+// registers and no LDS store instructions: each of the 512 threads moves two 16-byte
+// pieces per stage, one instruction filling 1 KB = 8 rows of 64 elements.  The rows are
+// unpadded; row R keeps its 16-byte chunk c at position c ^ ((R >> 1) & 7), so the 16
+// lanes of a fragment read (16 consecutive rows, one chunk) hit all 64 banks once.
+struct DmaWeights {
+  uint32_t voff[2];  // byte offset in the tile of this lane's chunk, per instruction
+  __device__ DmaWeights(int Kt, int wave, int lane) {
+#pragma unroll
+    for (int j = 0; j < 2; ++j) {
+      const int row = 8 * (2 * wave + j) + lane / 8;
+      const int c = (lane % 8) ^ ((row >> 1) & 7);
+      voff[j] = 2u * ((uint32_t)row * (uint32_t)Kt + 8u * c);
+    }
+  }
+  // Contraction columns k0 .. k0+63 of the tile into dst (128 x 64 elements).
+  __device__ __forceinline__ void copy(__amdgpu_buffer_rsrc_t tile, uint16_t* dst, int wave,
+                                       int k0) const {
+#pragma unroll
+    for (int j = 0; j < 2; ++j)
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(
+          tile, (__attribute__((address_space(3))) void*)(dst + (2 * wave + j) * 512), 16,
+          (int)voff[j], 2 * k0, 0, 0);
+  }
+};
+
+// stage_mfma over such a swizzled stage.  rowoff: element offset of the lane's gate row
+// per neuron block (the up row is 64 rows further); choff[s]: element offset of k-step
+// s's chunk within the row.
+template <int RB, int NB, bool ZERO>
+__device__ __forceinline__ void stage_mfma_swizzled(const uint16_t* B, const TokenRows<64, RB>& a,
+                                                    f32x16 (&acc)[RB][NB][2], const int (&rowoff)[NB],
+                                                    const int (&choff)[4]) {
+  constexpr int kSteps = 4, kAhead = 3;
+  bf16x8 frag[kAhead][NB][2];
+  auto read = [&](int buf, int s) __attribute__((always_inline)) {
+#pragma unroll
+    for (int nb = 0; nb < NB; ++nb) {
+      frag[buf][nb][0] = *reinterpret_cast<const bf16x8*>(B + rowoff[nb] + choff[s]);
+      frag[buf][nb][1] = *reinterpret_cast<const bf16x8*>(B + rowoff[nb] + kBN * 64 + choff[s]);
+    }
+  };
+#pragma unroll
+  for (int s = 0; s < kAhead; ++s) read(s, s);
+#pragma unroll
+  for (int s = 0; s < kSteps; ++s) {
+#pragma unroll
+    for (int nb = 0; nb < NB; ++nb)
+#pragma unroll
+      for (int rb = 0; rb < RB; ++rb) {
+        const bf16x8 av = __builtin_bit_cast(bf16x8, a.v[rb][s]);
+        const bool z = ZERO && s == 0;
+#pragma unroll
+        for (int gu = 0; gu < 2; ++gu)
+          acc[rb][nb][gu] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+              av, frag[s % kAhead][nb][gu], z ? f32x16{} : acc[rb][nb][gu], 0, 0, 0);
+      }
+    if (s + kAhead < kSteps) read(s % kAhead, s + kAhead);
+  }
+  constexpr int kFrags = 2 * NB, kMfma = 2 * NB * RB;
+  __builtin_amdgcn_sched_group_barrier(0x100, kAhead * kFrags, 0);
+#pragma unroll
+  for (int s = 0; s < kSteps; ++s) {
+    __builtin_amdgcn_sched_group_barrier(0x008, kMfma, 0);
+    if (s + kAhead < kSteps) __builtin_amdgcn_sched_group_barrier(0x100, kFrags, 0);
+  }
+}
+
 // Per-lane coefficients c1/p_t and c2/p_t of the accumulator elements, either as fp32 or
 // rounded to fp16 and packed as one 32-bit (c1, c2) pair (fp16 keeps 11 significant
 // bits, and the scaled coefficients lie within a factor 2 of silu'(g) u and silu(g)).
@@ -542,7 +610,14 @@ affinity_bf16_kernel(AffinityArgs p) {
   constexpr int kStageCols = 2 * kNeurons;
   static_assert(kNeurons % kBN == 0, "a block covers whole 64-neuron tiles");
   using WStage = WeightStage<KC, kStageCols, NT>;
-  __shared__ __attribute__((aligned(16))) uint16_t Bs[2][kStageCols * (KC + 8)];
+  // KC = 64 with one 64-neuron group: weight stages copied straight into LDS (DmaWeights),
+  // in two separate buffers, so the compiler can tell the reads of one stage from the copy
+  // into the other (one array indexed by the stage parity makes it wait for the copy
+  // before every read).  Otherwise through registers into a padded double buffer.
+  constexpr bool kDma = KC == 64 && kStageCols == 128 && NT == 512;
+  __shared__ __attribute__((aligned(16))) uint16_t Bs[2][kDma ? 8 : kStageCols * (KC + 8)];
+  __shared__ __attribute__((aligned(16))) uint16_t BsA[kDma ? kStageCols * KC : 8];
+  __shared__ __attribute__((aligned(16))) uint16_t BsB[kDma ? kStageCols * KC : 8];
   __shared__ __attribute__((aligned(16))) float rv[kRows];  // 1/r of the tile's rows, 0 past T
   __shared__ __attribute__((aligned(16))) float rv2[kRows];  // 1/r' of the rows (down statistic)
   extern __shared__ float red[];  // [WM*WN][G+1][32*NB]
@@ -579,6 +654,14 @@ affinity_bf16_kernel(AffinityArgs p) {
     gate_off[nb] = row * (KC + 8) + (lane >> 5) * (KC / 2);
     up_off[nb] = gate_off[nb] + kBN * (KC + 8);
   }
+  // The same fragments in the swizzled stage: the lane's row, and the position of k-step
+  // s's chunk (chunk 4 (lane / 32) + s, swizzled by the row).
+  int sw_row[NB], sw_chunk[4];
+#pragma unroll
+  for (int nb = 0; nb < NB; ++nb) sw_row[nb] = (32 * nb + (lane & 31)) * 64;
+#pragma unroll
+  for (int st = 0; st < 4; ++st) sw_chunk[st] = 8 * ((4 * (lane >> 5) + st) ^ (((lane & 31) >> 1) & 7));
+  const DmaWeights dma(p.Kt, wave, lane);
   __syncthreads();
 
   for (int mt = mt_begin; mt < mt_end; ++mt) {
@@ -603,30 +686,51 @@ affinity_bf16_kernel(AffinityArgs p) {
     TokenRows<KC, RB> t0, t1, t2;
     WStage w0, w1;
     load_tokens_for(t0, 0);
-    load_weights(w0, w_rsrc, w_off, 0);
+    if constexpr (!kDma) load_weights(w0, w_rsrc, w_off, 0);
     load_tokens_for(t1, min(1, nq - 1));
-    load_weights(w1, w_rsrc, w_off, min(1, nq - 1) * KC);
-    store_weights(w0, Bs[0]);
+    if constexpr (kDma) {
+      dma.copy(w_rsrc, BsA, wave, 0);
+    } else {
+      load_weights(w1, w_rsrc, w_off, min(1, nq - 1) * KC);
+      store_weights(w0, Bs[0]);
+    }
     for (int i = threadIdx.x; i < kRows; i += NT) {
       rv[i] = m0 + i < p.T ? p.rinv[m0 + i] : 0.0f;
       rv2[i] = down && m0 + i < p.T ? p.rinv_next[m0 + i] : 0.0f;
     }
+    if constexpr (kDma) __builtin_amdgcn_s_waitcnt(0x0f70);  // vmcnt(0): stage 0's copy landed
     __syncthreads();
 
     // Stage q: tokens in `cur`, stage q+1's weights in `wnext` (stored to LDS here),
     // stage q+2 fetched into `tnew` / `wnew`.
+    // In the copy mode bcur holds stage q's weights and stage q+1's are copied into bnxt,
+    // which stage q-1 read (free since the last barrier).
     auto stage = [&](int q, TokenRows<KC, RB>& cur, TokenRows<KC, RB>& tnew, WStage& wnext,
-                     WStage& wnew) __attribute__((always_inline)) {
+                     WStage& wnew, uint16_t* bcur, uint16_t* bnxt) __attribute__((always_inline)) {
       const int buf = q & 1;
       // Unconditional (the last two stages re-fetch the last stage), so that the wait
       // counts before each use stay exact instead of falling back to a full drain.
       const int qn = min(q + 2, nq - 1);
+      if constexpr (kDma) {
+        dma.copy(w_rsrc, bnxt, wave, min(q + 1, nq - 1) * KC);
+        // Keep the copy ahead of the token loads: the wait at the end of the stage counts
+        // on the loads issued after it.
+        __builtin_amdgcn_sched_barrier(0);
+      }
       load_tokens_for(tnew, qn);
-      load_weights(wnew, w_rsrc, w_off, qn * KC);
-      if (q == 0 || (q >= nq1 && head_stage == 0))
-        stage_mfma<KC, RB, NB, true>(Bs[buf], cur, acc, gate_off, up_off);
-      else
-        stage_mfma<KC, RB, NB, false>(Bs[buf], cur, acc, gate_off, up_off);
+      if constexpr (!kDma) load_weights(wnew, w_rsrc, w_off, qn * KC);
+      const bool zero = q == 0 || (q >= nq1 && head_stage == 0);
+      if constexpr (kDma) {
+        if (zero)
+          stage_mfma_swizzled<RB, NB, true>(bcur, cur, acc, sw_row, sw_chunk);
+        else
+          stage_mfma_swizzled<RB, NB, false>(bcur, cur, acc, sw_row, sw_chunk);
+      } else {
+        if (zero)
+          stage_mfma<KC, RB, NB, true>(Bs[buf], cur, acc, gate_off, up_off);
+        else
+          stage_mfma<KC, RB, NB, false>(Bs[buf], cur, acc, gate_off, up_off);
+      }
       if (q == nq1 - 1) {
         // Operating point: g, u -> c1 = silu'(g) u / r, c2 = silu(g) / r, stored divided
         // by p_t (the head entries were multiplied by it).  Lane l's element i is row
@@ -713,25 +817,34 @@ affinity_bf16_kernel(AffinityArgs p) {
         }
         ++h;
       }
-      store_weights(wnext, Bs[buf ^ 1]);  // unused after the last stage
-      __syncthreads();
+      if constexpr (kDma) {
+        // This wave's copy has landed once at most the RB * 4 token loads issued after it
+        // are outstanding (vmcnt), and its LDS reads are done (lgkmcnt 0); then the
+        // barrier.  __syncthreads() would also drain the token loads.
+        static_assert(RB * KC / 16 == 4, "the wait below counts four token loads per stage");
+        __builtin_amdgcn_s_waitcnt(0x0074);  // vmcnt(4) expcnt(7) lgkmcnt(0)
+        __builtin_amdgcn_s_barrier();
+      } else {
+        store_weights(wnext, Bs[buf ^ 1]);  // unused after the last stage
+        __syncthreads();
+      }
     };
 
     // Unrolled by six so the three token and two weight register sets rotate in place.
     int q = 0;
     for (; q + 5 < nq; q += 6) {
-      stage(q, t0, t2, w1, w0);
-      stage(q + 1, t1, t0, w0, w1);
-      stage(q + 2, t2, t1, w1, w0);
-      stage(q + 3, t0, t2, w0, w1);
-      stage(q + 4, t1, t0, w1, w0);
-      stage(q + 5, t2, t1, w0, w1);
+      stage(q, t0, t2, w1, w0, BsA, BsB);
+      stage(q + 1, t1, t0, w0, w1, BsB, BsA);
+      stage(q + 2, t2, t1, w1, w0, BsA, BsB);
+      stage(q + 3, t0, t2, w0, w1, BsB, BsA);
+      stage(q + 4, t1, t0, w1, w0, BsA, BsB);
+      stage(q + 5, t2, t1, w0, w1, BsB, BsA);
     }
-    if (q < nq) stage(q, t0, t2, w1, w0);
-    if (q + 1 < nq) stage(q + 1, t1, t0, w0, w1);
-    if (q + 2 < nq) stage(q + 2, t2, t1, w1, w0);
-    if (q + 3 < nq) stage(q + 3, t0, t2, w0, w1);
-    if (q + 4 < nq) stage(q + 4, t1, t0, w1, w0);
+    if (q < nq) stage(q, t0, t2, w1, w0, BsA, BsB);
+    if (q + 1 < nq) stage(q + 1, t1, t0, w0, w1, BsB, BsA);
+    if (q + 2 < nq) stage(q + 2, t2, t1, w1, w0, BsA, BsB);
+    if (q + 3 < nq) stage(q + 3, t0, t2, w0, w1, BsB, BsA);
+    if (q + 4 < nq) stage(q + 4, t1, t0, w1, w0, BsA, BsB);
   }
 
   // Sum the row waves in a fixed order and scale by ||w^d_k||^2.
