@@ -449,28 +449,34 @@ __device__ __forceinline__ void stage_mfma(const uint16_t* B, const TokenRows<KC
   }
 }
 
-// Weight stages of KC = 64 copied into LDS by the buffer unit (buffer_load ... lds), no
-// registers and no LDS store instructions: each of the 512 threads moves two 16-byte
-// pieces per stage, one instruction filling 1 KB = 8 rows of 64 elements.  The rows are
-// unpadded; row R keeps its 16-byte chunk c at position c ^ ((R >> 1) & 7), so the 16
-// lanes of a fragment read (16 consecutive rows, one chunk) hit all 64 banks once.
+// Weight stages of KC = 64 or 32 copied into LDS by the buffer unit (buffer_load ... lds),
+// no registers and no LDS store instructions: each instruction fills 1 KB of the 128-row
+// stage, KC / 32 instructions per thread of the 512.  The rows (KC elements) are
+// unpadded; row R keeps its 16-byte chunk c at position c ^ sw(R), with
+// sw(R) = (R / (128 / KC)) mod (KC / 8), so the 16 lanes of a fragment read (16
+// consecutive rows, one chunk) hit all 64 banks once.
+template <int KC>
 struct DmaWeights {
-  uint32_t voff[2];  // byte offset in the tile of this lane's chunk, per instruction
+  static constexpr int kChunks = KC / 8;        // 16-byte chunks per row
+  static constexpr int kRowsPerCopy = 512 / KC;  // rows per 1 KB instruction
+  static constexpr int kCopies = KC / 32;        // instructions per thread
+  __device__ static int swizzle(int row) { return (row / (128 / KC)) % kChunks; }
+  uint32_t voff[kCopies];  // byte offset in the tile of this lane's chunk, per instruction
   __device__ DmaWeights(int Kt, int wave, int lane) {
 #pragma unroll
-    for (int j = 0; j < 2; ++j) {
-      const int row = 8 * (2 * wave + j) + lane / 8;
-      const int c = (lane % 8) ^ ((row >> 1) & 7);
+    for (int j = 0; j < kCopies; ++j) {
+      const int row = kRowsPerCopy * (kCopies * wave + j) + lane / kChunks;
+      const int c = (lane % kChunks) ^ swizzle(row);
       voff[j] = 2u * ((uint32_t)row * (uint32_t)Kt + 8u * c);
     }
   }
-  // Contraction columns k0 .. k0+63 of the tile into dst (128 x 64 elements).
+  // Contraction columns k0 .. k0+KC-1 of the tile into dst (128 x KC elements).
   __device__ __forceinline__ void copy(__amdgpu_buffer_rsrc_t tile, uint16_t* dst, int wave,
                                        int k0) const {
 #pragma unroll
-    for (int j = 0; j < 2; ++j)
+    for (int j = 0; j < kCopies; ++j)
       __builtin_amdgcn_raw_ptr_buffer_load_lds(
-          tile, (__attribute__((address_space(3))) void*)(dst + (2 * wave + j) * 512), 16,
+          tile, (__attribute__((address_space(3))) void*)(dst + (kCopies * wave + j) * 512), 16,
           (int)voff[j], 2 * k0, 0, 0);
   }
 };
@@ -478,17 +484,18 @@ struct DmaWeights {
 // stage_mfma over such a swizzled stage.  rowoff: element offset of the lane's gate row
 // per neuron block (the up row is 64 rows further); choff[s]: element offset of k-step
 // s's chunk within the row.
-template <int RB, int NB, bool ZERO>
-__device__ __forceinline__ void stage_mfma_swizzled(const uint16_t* B, const TokenRows<64, RB>& a,
+template <int KC, int RB, int NB, bool ZERO>
+__device__ __forceinline__ void stage_mfma_swizzled(const uint16_t* B, const TokenRows<KC, RB>& a,
                                                     f32x16 (&acc)[RB][NB][2], const int (&rowoff)[NB],
-                                                    const int (&choff)[4]) {
-  constexpr int kSteps = 4, kAhead = 3;
+                                                    const int (&choff)[KC / 16]) {
+  constexpr int kSteps = KC / 16;
+  constexpr int kAhead = kSteps < 3 ? kSteps : 3;
   bf16x8 frag[kAhead][NB][2];
   auto read = [&](int buf, int s) __attribute__((always_inline)) {
 #pragma unroll
     for (int nb = 0; nb < NB; ++nb) {
       frag[buf][nb][0] = *reinterpret_cast<const bf16x8*>(B + rowoff[nb] + choff[s]);
-      frag[buf][nb][1] = *reinterpret_cast<const bf16x8*>(B + rowoff[nb] + kBN * 64 + choff[s]);
+      frag[buf][nb][1] = *reinterpret_cast<const bf16x8*>(B + rowoff[nb] + kBN * KC + choff[s]);
     }
   };
 #pragma unroll
@@ -610,11 +617,11 @@ affinity_bf16_kernel(AffinityArgs p) {
   constexpr int kStageCols = 2 * kNeurons;
   static_assert(kNeurons % kBN == 0, "a block covers whole 64-neuron tiles");
   using WStage = WeightStage<KC, kStageCols, NT>;
-  // KC = 64 with one 64-neuron group: weight stages copied straight into LDS (DmaWeights),
+  // KC = 64 or 32 with one 64-neuron group: weight stages copied straight into LDS (DmaWeights),
   // in two separate buffers, so the compiler can tell the reads of one stage from the copy
   // into the other (one array indexed by the stage parity makes it wait for the copy
   // before every read).  Otherwise through registers into a padded double buffer.
-  constexpr bool kDma = KC == 64 && kStageCols == 128 && NT == 512;
+  constexpr bool kDma = (KC == 64 || KC == 32) && kStageCols == 128 && NT == 512;
   __shared__ __attribute__((aligned(16))) uint16_t Bs[2][kDma ? 8 : kStageCols * (KC + 8)];
   __shared__ __attribute__((aligned(16))) uint16_t BsA[kDma ? kStageCols * KC : 8];
   __shared__ __attribute__((aligned(16))) uint16_t BsB[kDma ? kStageCols * KC : 8];
@@ -655,13 +662,15 @@ affinity_bf16_kernel(AffinityArgs p) {
     up_off[nb] = gate_off[nb] + kBN * (KC + 8);
   }
   // The same fragments in the swizzled stage: the lane's row, and the position of k-step
-  // s's chunk (chunk 4 (lane / 32) + s, swizzled by the row).
-  int sw_row[NB], sw_chunk[4];
+  // s's chunk (chunk (KC / 16) (lane / 32) + s, swizzled by the row; 32 nb and 64 are
+  // multiples of 16, so the swizzle depends on lane % 32 only).
+  int sw_row[NB], sw_chunk[KC / 16];
 #pragma unroll
-  for (int nb = 0; nb < NB; ++nb) sw_row[nb] = (32 * nb + (lane & 31)) * 64;
+  for (int nb = 0; nb < NB; ++nb) sw_row[nb] = (32 * nb + (lane & 31)) * KC;
 #pragma unroll
-  for (int st = 0; st < 4; ++st) sw_chunk[st] = 8 * ((4 * (lane >> 5) + st) ^ (((lane & 31) >> 1) & 7));
-  const DmaWeights dma(p.Kt, wave, lane);
+  for (int st = 0; st < KC / 16; ++st)
+    sw_chunk[st] = 8 * (((KC / 16) * (lane >> 5) + st) ^ DmaWeights<KC>::swizzle(lane & 31));
+  const DmaWeights<KC> dma(p.Kt, wave, lane);
   __syncthreads();
 
   for (int mt = mt_begin; mt < mt_end; ++mt) {
@@ -722,9 +731,9 @@ affinity_bf16_kernel(AffinityArgs p) {
       const bool zero = q == 0 || (q >= nq1 && head_stage == 0);
       if constexpr (kDma) {
         if (zero)
-          stage_mfma_swizzled<RB, NB, true>(bcur, cur, acc, sw_row, sw_chunk);
+          stage_mfma_swizzled<KC, RB, NB, true>(bcur, cur, acc, sw_row, sw_chunk);
         else
-          stage_mfma_swizzled<RB, NB, false>(bcur, cur, acc, sw_row, sw_chunk);
+          stage_mfma_swizzled<KC, RB, NB, false>(bcur, cur, acc, sw_row, sw_chunk);
       } else {
         if (zero)
           stage_mfma<KC, RB, NB, true>(Bs[buf], cur, acc, gate_off, up_off);
@@ -818,11 +827,12 @@ affinity_bf16_kernel(AffinityArgs p) {
         ++h;
       }
       if constexpr (kDma) {
-        // This wave's copy has landed once at most the RB * 4 token loads issued after it
-        // are outstanding (vmcnt), and its LDS reads are done (lgkmcnt 0); then the
-        // barrier.  __syncthreads() would also drain the token loads.
-        static_assert(RB * KC / 16 == 4, "the wait below counts four token loads per stage");
-        __builtin_amdgcn_s_waitcnt(0x0074);  // vmcnt(4) expcnt(7) lgkmcnt(0)
+        // This wave's copy has landed once at most the RB * KC / 16 token loads issued
+        // after it are outstanding (vmcnt), and its LDS reads are done (lgkmcnt 0); then
+        // the barrier.  __syncthreads() would also drain the token loads.
+        constexpr int kLater = RB * KC / 16;
+        static_assert(kLater < 16, "vmcnt field");
+        __builtin_amdgcn_s_waitcnt(0x0070 | kLater);  // vmcnt(kLater) expcnt(7) lgkmcnt(0)
         __builtin_amdgcn_s_barrier();
       } else {
         store_weights(wnext, Bs[buf ^ 1]);  // unused after the last stage
