@@ -625,6 +625,7 @@ affinity_bf16_kernel(AffinityArgs p) {
   __shared__ __attribute__((aligned(16))) uint16_t Bs[2][kDma ? 8 : kStageCols * (KC + 8)];
   __shared__ __attribute__((aligned(16))) uint16_t BsA[kDma ? kStageCols * KC : 8];
   __shared__ __attribute__((aligned(16))) uint16_t BsB[kDma ? kStageCols * KC : 8];
+  __shared__ __attribute__((aligned(16))) uint16_t BsC[kDma ? kStageCols * KC : 8];
   __shared__ __attribute__((aligned(16))) float rv[kRows];  // 1/r of the tile's rows, 0 past T
   __shared__ __attribute__((aligned(16))) float rv2[kRows];  // 1/r' of the rows (down statistic)
   extern __shared__ float red[];  // [WM*WN][G+1][32*NB]
@@ -699,6 +700,7 @@ affinity_bf16_kernel(AffinityArgs p) {
     load_tokens_for(t1, min(1, nq - 1));
     if constexpr (kDma) {
       dma.copy(w_rsrc, BsA, wave, 0);
+      dma.copy(w_rsrc, BsB, wave, min(1, nq - 1) * KC);
     } else {
       load_weights(w1, w_rsrc, w_off, min(1, nq - 1) * KC);
       store_weights(w0, Bs[0]);
@@ -712,8 +714,9 @@ affinity_bf16_kernel(AffinityArgs p) {
 
     // Stage q: tokens in `cur`, stage q+1's weights in `wnext` (stored to LDS here),
     // stage q+2 fetched into `tnew` / `wnew`.
-    // In the copy mode bcur holds stage q's weights and stage q+1's are copied into bnxt,
-    // which stage q-1 read (free since the last barrier).
+    // In the copy mode three buffers rotate: bcur holds stage q's weights, stage q+1's
+    // are in flight or landed, and stage q+2's are copied into bnxt, which stage q-1 read
+    // (free since the last barrier).
     auto stage = [&](int q, TokenRows<KC, RB>& cur, TokenRows<KC, RB>& tnew, WStage& wnext,
                      WStage& wnew, uint16_t* bcur, uint16_t* bnxt) __attribute__((always_inline)) {
       const int buf = q & 1;
@@ -721,7 +724,7 @@ affinity_bf16_kernel(AffinityArgs p) {
       // counts before each use stay exact instead of falling back to a full drain.
       const int qn = min(q + 2, nq - 1);
       if constexpr (kDma) {
-        dma.copy(w_rsrc, bnxt, wave, min(q + 1, nq - 1) * KC);
+        dma.copy(w_rsrc, bnxt, wave, min(q + 2, nq - 1) * KC);
         // Keep the copy ahead of the token loads: the wait at the end of the stage counts
         // on the loads issued after it.
         __builtin_amdgcn_sched_barrier(0);
@@ -827,10 +830,11 @@ affinity_bf16_kernel(AffinityArgs p) {
         ++h;
       }
       if constexpr (kDma) {
-        // This wave's copy has landed once at most the RB * KC / 16 token loads issued
-        // after it are outstanding (vmcnt), and its LDS reads are done (lgkmcnt 0); then
-        // the barrier.  __syncthreads() would also drain the token loads.
-        constexpr int kLater = RB * KC / 16;
+        // Stage q+1's copy (issued at the start of stage q-1) has landed for this wave once
+        // at most the loads issued after it are outstanding: its stage's token loads, then
+        // this stage's copy and token loads (vmcnt); this wave's LDS reads are done
+        // (lgkmcnt 0); then the barrier.  __syncthreads() would drain every load.
+        constexpr int kLater = 2 * (RB * KC / 16) + DmaWeights<KC>::kCopies;
         static_assert(kLater < 16, "vmcnt field");
         __builtin_amdgcn_s_waitcnt(0x0070 | kLater);  // vmcnt(kLater) expcnt(7) lgkmcnt(0)
         __builtin_amdgcn_s_barrier();
@@ -843,18 +847,18 @@ affinity_bf16_kernel(AffinityArgs p) {
     // Unrolled by six so the three token and two weight register sets rotate in place.
     int q = 0;
     for (; q + 5 < nq; q += 6) {
-      stage(q, t0, t2, w1, w0, BsA, BsB);
+      stage(q, t0, t2, w1, w0, BsA, BsC);
       stage(q + 1, t1, t0, w0, w1, BsB, BsA);
-      stage(q + 2, t2, t1, w1, w0, BsA, BsB);
-      stage(q + 3, t0, t2, w0, w1, BsB, BsA);
-      stage(q + 4, t1, t0, w1, w0, BsA, BsB);
-      stage(q + 5, t2, t1, w0, w1, BsB, BsA);
+      stage(q + 2, t2, t1, w1, w0, BsC, BsB);
+      stage(q + 3, t0, t2, w0, w1, BsA, BsC);
+      stage(q + 4, t1, t0, w1, w0, BsB, BsA);
+      stage(q + 5, t2, t1, w0, w1, BsC, BsB);
     }
-    if (q < nq) stage(q, t0, t2, w1, w0, BsA, BsB);
+    if (q < nq) stage(q, t0, t2, w1, w0, BsA, BsC);
     if (q + 1 < nq) stage(q + 1, t1, t0, w0, w1, BsB, BsA);
-    if (q + 2 < nq) stage(q + 2, t2, t1, w1, w0, BsA, BsB);
-    if (q + 3 < nq) stage(q + 3, t0, t2, w0, w1, BsB, BsA);
-    if (q + 4 < nq) stage(q + 4, t1, t0, w1, w0, BsA, BsB);
+    if (q + 2 < nq) stage(q + 2, t2, t1, w1, w0, BsC, BsB);
+    if (q + 3 < nq) stage(q + 3, t0, t2, w0, w1, BsA, BsC);
+    if (q + 4 < nq) stage(q + 4, t1, t0, w1, w0, BsB, BsA);
   }
 
   // Sum the row waves in a fixed order and scale by ||w^d_k||^2.
