@@ -44,6 +44,9 @@ def oracle(wl, w, x, a, neurons=None):
     ("qwen3-0.6b-layer", 129, dict(n_q_heads=8, n_kv_groups=8, head_dim=48)),  # H = G, dh % 32 = 16
     ("qwen3-0.6b-layer", 100, dict(n_q_heads=32, n_kv_groups=32, head_dim=64)),  # G at its limit
     ("danube3-500m", 64, dict(d_model=272, n_neurons=192)),         # d % 32 = 16
+    # two 64-deep stages and two 32-deep stages: the three-buffer weight ring wraps early
+    ("qwen3-0.6b-layer", 70, dict(d_model=64, n_q_heads=1, n_kv_groups=1, head_dim=64, n_neurons=128)),
+    ("danube3-500m", 40, dict(d_model=32, n_q_heads=1, n_kv_groups=1, head_dim=32, n_neurons=64)),
 ])
 def test_affinity_matches_oracle(name, T, shape):
     wl, w, x, a = case(name, T, **shape)
