@@ -601,9 +601,11 @@ __device__ __forceinline__ void block_work(int b, int n_tg, int n_split, int& tg
 // Kt = d + H*dh in stages of KC:
 //   stages [0, d/KC)          acc = [x] . [W'_gate | W'_up]^T          -> c1, c2 in registers
 //   each next dh/KC stages    acc = [a_h] . [Fg_h | Fu_h]^T            -> Delta^2 column sums
-// Both operands are fetched two stages ahead into registers: the token fragments (one
-// contiguous 1 KB load per k-step) go straight to the MFMAs, the weight stage shared by
-// the block is written to a double-buffered LDS tile one stage before use, and each LDS
+// The token fragments (one contiguous 1 KB load per k-step) are fetched two stages ahead
+// into registers and go straight to the MFMAs.  The weight stage shared by the block goes
+// through LDS: at KC = 64 and 32 copied there by the buffer unit two stages ahead into a
+// ring of three swizzled buffers (DmaWeights), otherwise fetched into registers two
+// stages ahead and stored into a padded double buffer one stage before use.  Each LDS
 // fragment feeds RB MFMAs.  Rows past the last token get zero coefficients.  Column sums
 // are kept per lane over its rows, folded across the two half-waves after the last query
 // head of each KV group, and banked in LDS per (wave, group); the block writes the
@@ -712,7 +714,8 @@ affinity_bf16_kernel(AffinityArgs p) {
     if constexpr (kDma) __builtin_amdgcn_s_waitcnt(0x0f70);  // vmcnt(0): stage 0's copy landed
     __syncthreads();
 
-    // Stage q: tokens in `cur`, stage q+1's weights in `wnext` (stored to LDS here),
+    // Stage q: tokens in `cur`, stage q+1's weights in `wnext` (stored to LDS here unless
+    // they are copied),
     // stage q+2 fetched into `tnew` / `wnew`.
     // In the copy mode three buffers rotate: bcur holds stage q's weights, stage q+1's
     // are in flight or landed, and stage q+2's are copied into bnxt, which stage q-1 read
@@ -844,7 +847,8 @@ affinity_bf16_kernel(AffinityArgs p) {
       }
     };
 
-    // Unrolled by six so the three token and two weight register sets rotate in place.
+    // Unrolled by six so the three token and two weight register sets, and the three
+    // copy buffers, rotate in place.
     int q = 0;
     for (; q + 5 < nq; q += 6) {
       stage(q, t0, t2, w1, w0, BsA, BsC);
