@@ -48,6 +48,7 @@ constexpr int kSliceTokens = 1 << 18;  // tokens per internal slice (size of the
 constexpr int kMaxSplits = 128;        // token splits per launch (size of the partials)
 constexpr int kTileTokens = 1 << 15;   // tokens per bf16 slice (size of the tiled token buffer)
 constexpr int kTargetBlocks = 3072;    // aim for this many blocks per launch
+constexpr size_t kLdsPerCu = 160 * 1024;  // LDS bytes per CU (gfx950)
 
 template <typename T>
 __device__ inline float load_f32(const T* p, int64_t i);
@@ -610,7 +611,7 @@ __device__ __forceinline__ void block_work(int b, int n_tg, int n_split, int& tg
 // are kept per lane over its rows, folded across the two half-waves after the last query
 // head of each KV group, and banked in LDS per (wave, group); the block writes the
 // fixed-order sum over its WM row waves times ||w^d_k||^2 to its split's partial.
-template <int KC, int WM, int WN, int RB, int NB, bool PACK, int SG, bool ADD>
+template <int KC, int WM, int WN, int RB, int NB, bool PACK, int SG, bool ADD, int RING>
 __global__ void __launch_bounds__(64 * WM * WN, 2)  // two waves per SIMD
 affinity_bf16_kernel(AffinityArgs p) {
   constexpr int NT = 64 * WM * WN;
@@ -624,10 +625,17 @@ affinity_bf16_kernel(AffinityArgs p) {
   // into the other (one array indexed by the stage parity makes it wait for the copy
   // before every read).  Otherwise through registers into a padded double buffer.
   constexpr bool kDma = (KC == 64 || KC == 32) && kStageCols == 128 && NT == 512;
+  // Copied stages rotate through RING buffers: with three, every stage ends at a barrier;
+  // with six, every second one does (stage q+3 is copied during stage q).
+  static_assert(RING == 3 || (RING == 6 && kDma), "three or six copy buffers");
+  constexpr bool kPairs = RING == 6;
   __shared__ __attribute__((aligned(16))) uint16_t Bs[2][kDma ? 8 : kStageCols * (KC + 8)];
   __shared__ __attribute__((aligned(16))) uint16_t BsA[kDma ? kStageCols * KC : 8];
   __shared__ __attribute__((aligned(16))) uint16_t BsB[kDma ? kStageCols * KC : 8];
   __shared__ __attribute__((aligned(16))) uint16_t BsC[kDma ? kStageCols * KC : 8];
+  __shared__ __attribute__((aligned(16))) uint16_t BsD[kPairs ? kStageCols * KC : 8];
+  __shared__ __attribute__((aligned(16))) uint16_t BsE[kPairs ? kStageCols * KC : 8];
+  __shared__ __attribute__((aligned(16))) uint16_t BsF[kPairs ? kStageCols * KC : 8];
   __shared__ __attribute__((aligned(16))) float rv[kRows];  // 1/r of the tile's rows, 0 past T
   __shared__ __attribute__((aligned(16))) float rv2[kRows];  // 1/r' of the rows (down statistic)
   extern __shared__ float red[];  // [WM*WN][G+1][32*NB]
@@ -703,6 +711,7 @@ affinity_bf16_kernel(AffinityArgs p) {
     if constexpr (kDma) {
       dma.copy(w_rsrc, BsA, wave, 0);
       dma.copy(w_rsrc, BsB, wave, min(1, nq - 1) * KC);
+      if constexpr (kPairs) dma.copy(w_rsrc, BsC, wave, min(2, nq - 1) * KC);
     } else {
       load_weights(w1, w_rsrc, w_off, min(1, nq - 1) * KC);
       store_weights(w0, Bs[0]);
@@ -717,17 +726,21 @@ affinity_bf16_kernel(AffinityArgs p) {
     // Stage q: tokens in `cur`, stage q+1's weights in `wnext` (stored to LDS here unless
     // they are copied),
     // stage q+2 fetched into `tnew` / `wnew`.
-    // In the copy mode three buffers rotate: bcur holds stage q's weights, stage q+1's
-    // are in flight or landed, and stage q+2's are copied into bnxt, which stage q-1 read
-    // (free since the last barrier).
+    // In the copy mode with three buffers: bcur holds stage q's weights, stage q+1's are
+    // in flight or landed, and stage q+2's are copied into bnxt, which stage q-1 read (free
+    // since the last barrier).  With six, barriers end the odd stages only, so during
+    // stages 2p and 2p+1 every wave is within those two: stage q+3 is copied into the
+    // buffer of stage q-3, which all waves left before the last barrier, and the barrier
+    // after stage 2p+1 waits for the copies of stages 2p+2 and 2p+3.  `odd`: the stage
+    // ends a pair (with three buffers, every stage is passed true).
     auto stage = [&](int q, TokenRows<KC, RB>& cur, TokenRows<KC, RB>& tnew, WStage& wnext,
-                     WStage& wnew, uint16_t* bcur, uint16_t* bnxt) __attribute__((always_inline)) {
+                     WStage& wnew, uint16_t* bcur, uint16_t* bnxt, bool odd) __attribute__((always_inline)) {
       const int buf = q & 1;
       // Unconditional (the last two stages re-fetch the last stage), so that the wait
       // counts before each use stay exact instead of falling back to a full drain.
       const int qn = min(q + 2, nq - 1);
       if constexpr (kDma) {
-        dma.copy(w_rsrc, bnxt, wave, min(q + 2, nq - 1) * KC);
+        dma.copy(w_rsrc, bnxt, wave, min(q + (kPairs ? 3 : 2), nq - 1) * KC);
         // Keep the copy ahead of the token loads: the wait at the end of the stage counts
         // on the loads issued after it.
         __builtin_amdgcn_sched_barrier(0);
@@ -833,36 +846,55 @@ affinity_bf16_kernel(AffinityArgs p) {
         ++h;
       }
       if constexpr (kDma) {
-        // Stage q+1's copy (issued at the start of stage q-1) has landed for this wave once
-        // at most the loads issued after it are outstanding: its stage's token loads, then
-        // this stage's copy and token loads (vmcnt); this wave's LDS reads are done
-        // (lgkmcnt 0); then the barrier.  __syncthreads() would drain every load.
+        // Stage q+1's copy (issued at the start of stage q-1; with six buffers stage q+2's,
+        // issued at the start of stage q-1) has landed for this wave once at most the loads
+        // issued after it are outstanding: its stage's token loads, then this stage's copy
+        // and token loads (vmcnt); this wave's LDS reads are done (lgkmcnt 0); then the
+        // barrier.  __syncthreads() would drain every load.
         constexpr int kLater = 2 * (RB * KC / 16) + DmaWeights<KC>::kCopies;
         static_assert(kLater < 16, "vmcnt field");
-        __builtin_amdgcn_s_waitcnt(0x0070 | kLater);  // vmcnt(kLater) expcnt(7) lgkmcnt(0)
-        __builtin_amdgcn_s_barrier();
+        if (!kPairs || odd || q == nq - 1) {
+          __builtin_amdgcn_s_waitcnt(0x0070 | kLater);  // vmcnt(kLater) expcnt(7) lgkmcnt(0)
+          __builtin_amdgcn_s_barrier();
+        }
       } else {
         store_weights(wnext, Bs[buf ^ 1]);  // unused after the last stage
         __syncthreads();
       }
     };
 
-    // Unrolled by six so the three token and two weight register sets, and the three
-    // copy buffers, rotate in place.
+    // Unrolled by six so the three token and two weight register sets, and the three or
+    // six copy buffers, rotate in place.
     int q = 0;
-    for (; q + 5 < nq; q += 6) {
-      stage(q, t0, t2, w1, w0, BsA, BsC);
-      stage(q + 1, t1, t0, w0, w1, BsB, BsA);
-      stage(q + 2, t2, t1, w1, w0, BsC, BsB);
-      stage(q + 3, t0, t2, w0, w1, BsA, BsC);
-      stage(q + 4, t1, t0, w1, w0, BsB, BsA);
-      stage(q + 5, t2, t1, w0, w1, BsC, BsB);
+    if constexpr (kPairs) {
+      for (; q + 5 < nq; q += 6) {
+        stage(q, t0, t2, w1, w0, BsA, BsD, false);
+        stage(q + 1, t1, t0, w0, w1, BsB, BsE, true);
+        stage(q + 2, t2, t1, w1, w0, BsC, BsF, false);
+        stage(q + 3, t0, t2, w0, w1, BsD, BsA, true);
+        stage(q + 4, t1, t0, w1, w0, BsE, BsB, false);
+        stage(q + 5, t2, t1, w0, w1, BsF, BsC, true);
+      }
+      if (q < nq) stage(q, t0, t2, w1, w0, BsA, BsD, false);
+      if (q + 1 < nq) stage(q + 1, t1, t0, w0, w1, BsB, BsE, true);
+      if (q + 2 < nq) stage(q + 2, t2, t1, w1, w0, BsC, BsF, false);
+      if (q + 3 < nq) stage(q + 3, t0, t2, w0, w1, BsD, BsA, true);
+      if (q + 4 < nq) stage(q + 4, t1, t0, w1, w0, BsE, BsB, false);
+    } else {
+      for (; q + 5 < nq; q += 6) {
+        stage(q, t0, t2, w1, w0, BsA, BsC, true);
+        stage(q + 1, t1, t0, w0, w1, BsB, BsA, true);
+        stage(q + 2, t2, t1, w1, w0, BsC, BsB, true);
+        stage(q + 3, t0, t2, w0, w1, BsA, BsC, true);
+        stage(q + 4, t1, t0, w1, w0, BsB, BsA, true);
+        stage(q + 5, t2, t1, w0, w1, BsC, BsB, true);
+      }
+      if (q < nq) stage(q, t0, t2, w1, w0, BsA, BsC, true);
+      if (q + 1 < nq) stage(q + 1, t1, t0, w0, w1, BsB, BsA, true);
+      if (q + 2 < nq) stage(q + 2, t2, t1, w1, w0, BsC, BsB, true);
+      if (q + 3 < nq) stage(q + 3, t0, t2, w0, w1, BsA, BsC, true);
+      if (q + 4 < nq) stage(q + 4, t1, t0, w1, w0, BsB, BsA, true);
     }
-    if (q < nq) stage(q, t0, t2, w1, w0, BsA, BsC);
-    if (q + 1 < nq) stage(q + 1, t1, t0, w0, w1, BsB, BsA);
-    if (q + 2 < nq) stage(q + 2, t2, t1, w1, w0, BsC, BsB);
-    if (q + 3 < nq) stage(q + 3, t0, t2, w0, w1, BsA, BsC);
-    if (q + 4 < nq) stage(q + 4, t1, t0, w1, w0, BsB, BsA);
   }
 
   // Sum the row waves in a fixed order and scale by ||w^d_k||^2.
@@ -876,20 +908,53 @@ affinity_bf16_kernel(AffinityArgs p) {
   }
 }
 
-// Launches the fused kernel on one slice; returns the number of token splits used.
-template <int KC, int WM, int WN, int RB, int NB, bool PACK = false, int SG = 4, bool ADD = false>
+// Dynamic LDS of the fused kernel: the per-wave group sums.
+template <int WM, int WN, int NB>
+size_t affinity_dynamic_lds(int G) {
+  return sizeof(float) * WM * WN * (G + 1) * 32 * NB;
+}
+
+// Whether a block of the kernel fits one CU's LDS, less `margin`, with `dynamic` bytes on
+// top of its static arrays.  A block that fits no CU would never be scheduled and the
+// launch would never finish, so launches check this first.  The static size is the
+// larger of what the runtime reports and the sum of the copy buffers.
+template <int KC, int WM, int WN, int RB, int NB, bool PACK, int SG, bool ADD, int RING>
+bool affinity_lds_fits(size_t dynamic, size_t margin = 0) {
+  static const size_t static_lds = [] {
+    hipFuncAttributes a{};
+    const hipError_t e = hipFuncGetAttributes(
+        &a, (const void*)&affinity_bf16_kernel<KC, WM, WN, RB, NB, PACK, SG, ADD, RING>);
+    const size_t buffers = sizeof(uint16_t) * RING * (2 * 32 * NB * WN) * KC;
+    return e == hipSuccess ? std::max(a.sharedSizeBytes, buffers) : ~size_t(0) / 2;
+  }();
+  return static_lds + dynamic + margin <= kLdsPerCu;
+}
+
+// Launches the fused kernel on one slice; returns the number of token splits used, or 0
+// if a block does not fit the LDS.
+template <int KC, int WM, int WN, int RB, int NB, bool PACK, int SG, bool ADD, int RING>
 int launch_affinity(AffinityArgs p, hipStream_t s) {
   constexpr int kRows = 32 * RB * WM;
   constexpr int kNeurons = 32 * NB * WN;
   const int groups = p.n_tiles * kBN / kNeurons;
   const int mtiles = (p.T + kRows - 1) / kRows;
   p.splits = std::max(1, std::min((kTargetBlocks + groups - 1) / groups, std::min(mtiles, kMaxSplits)));
-  const size_t shm = sizeof(float) * WM * WN * (p.G + 1) * 32 * NB;
+  const size_t shm = affinity_dynamic_lds<WM, WN, NB>(p.G);
+  if (!affinity_lds_fits<KC, WM, WN, RB, NB, PACK, SG, ADD, RING>(shm)) return 0;
   if (shm > 65536)  // beyond the default dynamic LDS limit (G close to 32)
-    (void)hipFuncSetAttribute((const void*)&affinity_bf16_kernel<KC, WM, WN, RB, NB, PACK, SG, ADD>,
+    (void)hipFuncSetAttribute((const void*)&affinity_bf16_kernel<KC, WM, WN, RB, NB, PACK, SG, ADD, RING>,
                               hipFuncAttributeMaxDynamicSharedMemorySize, (int)shm);
-  affinity_bf16_kernel<KC, WM, WN, RB, NB, PACK, SG, ADD><<<groups * p.splits, 64 * WM * WN, shm, s>>>(p);
+  affinity_bf16_kernel<KC, WM, WN, RB, NB, PACK, SG, ADD, RING><<<groups * p.splits, 64 * WM * WN, shm, s>>>(p);
   return p.splits;
+}
+
+// The 64- and 32-deep kernels with six copy buffers where the block fits the LDS with 8 KB
+// to spare (G up to 26 at KC = 64), else with three.
+template <int KC, bool ADD>
+int launch_affinity_copied(AffinityArgs p, hipStream_t s) {
+  if (affinity_lds_fits<KC, 8, 1, 1, 2, true, 4, ADD, 6>(affinity_dynamic_lds<8, 1, 2>(p.G), 8192))
+    return launch_affinity<KC, 8, 1, 1, 2, true, 4, ADD, 6>(p, s);
+  return launch_affinity<KC, 8, 1, 1, 2, true, 4, ADD, 3>(p, s);
 }
 
 // ------------------------------------------------------------------ fused affinity (fp32)
@@ -1159,14 +1224,14 @@ dtp_status accumulate(dtp_layer L, const void* x, const void* attn, const void* 
       // Eight wavefronts per block (one block per CU): 256 tokens x 64 neurons per tile;
       // four for 16-wide stages, whose weight stage has only 256 16-byte pieces.
       if (kc == 64)
-        splits = add ? launch_affinity<64, 8, 1, 1, 2, true, 4, true>(p, s)
-                     : launch_affinity<64, 8, 1, 1, 2, true, 4, false>(p, s);
+        splits = add ? launch_affinity_copied<64, true>(p, s) : launch_affinity_copied<64, false>(p, s);
       else if (kc == 32)
-        splits = add ? launch_affinity<32, 8, 1, 1, 2, true, 4, true>(p, s)
-                     : launch_affinity<32, 8, 1, 1, 2, true, 4, false>(p, s);
+        splits = add ? launch_affinity_copied<32, true>(p, s) : launch_affinity_copied<32, false>(p, s);
       else
-        splits = add ? launch_affinity<16, 4, 1, 1, 2, true, 4, true>(p, s)
-                     : launch_affinity<16, 4, 1, 1, 2, true, 4, false>(p, s);
+        splits = add ? launch_affinity<16, 4, 1, 1, 2, true, 4, true, 3>(p, s)
+                     : launch_affinity<16, 4, 1, 1, 2, true, 4, false, 3>(p, s);
+      DTP_CHECK(splits > 0, DTP_ERR_UNSUPPORTED,
+                "affinity kernel: %d groups need more LDS than a CU holds", G);
     } else {
       splits = (kTargetBlocks / 4 + L->n_tiles - 1) / L->n_tiles;
       splits = std::max(1, std::min(splits, std::min(T, kMaxSplits)));

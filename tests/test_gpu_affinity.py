@@ -43,10 +43,16 @@ def oracle(wl, w, x, a, neurons=None):
     ("qwen3-0.6b-layer", 130, dict(n_q_heads=2, n_kv_groups=1)),    # one group
     ("qwen3-0.6b-layer", 129, dict(n_q_heads=8, n_kv_groups=8, head_dim=48)),  # H = G, dh % 32 = 16
     ("qwen3-0.6b-layer", 100, dict(n_q_heads=32, n_kv_groups=32, head_dim=64)),  # G at its limit
+    # the largest G with six copy buffers in the LDS, and the smallest that falls back to three
+    ("qwen3-0.6b-layer", 90, dict(n_q_heads=26, n_kv_groups=26, head_dim=64)),
+    ("qwen3-0.6b-layer", 90, dict(n_q_heads=27, n_kv_groups=27, head_dim=64)),
     ("danube3-500m", 64, dict(d_model=272, n_neurons=192)),         # d % 32 = 16
-    # two 64-deep stages and two 32-deep stages: the three-buffer weight ring wraps early
+    # two 64-deep stages and two 32-deep stages: the weight ring wraps within a tile
     ("qwen3-0.6b-layer", 70, dict(d_model=64, n_q_heads=1, n_kv_groups=1, head_dim=64, n_neurons=128)),
     ("danube3-500m", 40, dict(d_model=32, n_q_heads=1, n_kv_groups=1, head_dim=32, n_neurons=64)),
+    # an odd number of stages (three), so the last one ends an unfinished pair of stages
+    ("qwen3-0.6b-layer", 600, dict(d_model=128, n_q_heads=1, n_kv_groups=1, head_dim=64, n_neurons=128)),
+    ("danube3-500m", 300, dict(d_model=64, n_q_heads=1, n_kv_groups=1, head_dim=32, n_neurons=64)),
 ])
 def test_affinity_matches_oracle(name, T, shape):
     wl, w, x, a = case(name, T, **shape)
