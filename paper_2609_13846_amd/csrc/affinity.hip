@@ -604,8 +604,8 @@ __device__ __forceinline__ void block_work(int b, int n_tg, int n_split, int& tg
 //   each next dh/KC stages    acc = [a_h] . [Fg_h | Fu_h]^T            -> Delta^2 column sums
 // The token fragments (one contiguous 1 KB load per k-step) are fetched two stages ahead
 // into registers and go straight to the MFMAs.  The weight stage shared by the block goes
-// through LDS: at KC = 64 and 32 copied there by the buffer unit two stages ahead into a
-// ring of three swizzled buffers (DmaWeights), otherwise fetched into registers two
+// through LDS: at KC = 64 and 32 copied there by the buffer unit two or three stages ahead
+// into a ring of three or six swizzled buffers (DmaWeights), otherwise fetched into registers two
 // stages ahead and stored into a padded double buffer one stage before use.  Each LDS
 // fragment feeds RB MFMAs.  Rows past the last token get zero coefficients.  Column sums
 // are kept per lane over its rows, folded across the two half-waves after the last query
@@ -728,13 +728,15 @@ affinity_bf16_kernel(AffinityArgs p) {
     // stage q+2 fetched into `tnew` / `wnew`.
     // In the copy mode with three buffers: bcur holds stage q's weights, stage q+1's are
     // in flight or landed, and stage q+2's are copied into bnxt, which stage q-1 read (free
-    // since the last barrier).  With six, barriers end the odd stages only, so during
-    // stages 2p and 2p+1 every wave is within those two: stage q+3 is copied into the
+    // since the last barrier).  With six, barriers end the even stages only, so during
+    // stages 2p-1 and 2p every wave is within those two: stage q+3 is copied into the
     // buffer of stage q-3, which all waves left before the last barrier, and the barrier
-    // after stage 2p+1 waits for the copies of stages 2p+2 and 2p+3.  `odd`: the stage
-    // ends a pair (with three buffers, every stage is passed true).
+    // after stage 2p waits for the copies of stages 2p+1 and 2p+2.  A head of two stages
+    // then ends with no barrier after its epilogue, so one wave's epilogue can run beside
+    // the other wave's next MFMAs.  `sync`: the stage ends at a barrier (with three
+    // buffers, every stage does).
     auto stage = [&](int q, TokenRows<KC, RB>& cur, TokenRows<KC, RB>& tnew, WStage& wnext,
-                     WStage& wnew, uint16_t* bcur, uint16_t* bnxt, bool odd) __attribute__((always_inline)) {
+                     WStage& wnew, uint16_t* bcur, uint16_t* bnxt, bool sync) __attribute__((always_inline)) {
       const int buf = q & 1;
       // Unconditional (the last two stages re-fetch the last stage), so that the wait
       // counts before each use stay exact instead of falling back to a full drain.
@@ -846,14 +848,15 @@ affinity_bf16_kernel(AffinityArgs p) {
         ++h;
       }
       if constexpr (kDma) {
-        // Stage q+1's copy (issued at the start of stage q-1; with six buffers stage q+2's,
-        // issued at the start of stage q-1) has landed for this wave once at most the loads
-        // issued after it are outstanding: its stage's token loads, then this stage's copy
-        // and token loads (vmcnt); this wave's LDS reads are done (lgkmcnt 0); then the
-        // barrier.  __syncthreads() would drain every load.
+        // The copies the next stages read (stage q+1's; with six buffers also stage q+2's)
+        // have landed for this wave once at most the loads issued after the last of them
+        // are outstanding.  That one was issued at the start of stage q-1, and after it
+        // came stage q-1's token loads, then this stage's copy and token loads (vmcnt);
+        // this wave's LDS reads are done (lgkmcnt 0); then the barrier.  __syncthreads()
+        // would drain every load.
         constexpr int kLater = 2 * (RB * KC / 16) + DmaWeights<KC>::kCopies;
         static_assert(kLater < 16, "vmcnt field");
-        if (!kPairs || odd || q == nq - 1) {
+        if (!kPairs || sync || q == nq - 1) {
           __builtin_amdgcn_s_waitcnt(0x0070 | kLater);  // vmcnt(kLater) expcnt(7) lgkmcnt(0)
           __builtin_amdgcn_s_barrier();
         }
@@ -868,18 +871,18 @@ affinity_bf16_kernel(AffinityArgs p) {
     int q = 0;
     if constexpr (kPairs) {
       for (; q + 5 < nq; q += 6) {
-        stage(q, t0, t2, w1, w0, BsA, BsD, false);
-        stage(q + 1, t1, t0, w0, w1, BsB, BsE, true);
-        stage(q + 2, t2, t1, w1, w0, BsC, BsF, false);
-        stage(q + 3, t0, t2, w0, w1, BsD, BsA, true);
-        stage(q + 4, t1, t0, w1, w0, BsE, BsB, false);
-        stage(q + 5, t2, t1, w0, w1, BsF, BsC, true);
+        stage(q, t0, t2, w1, w0, BsA, BsD, true);
+        stage(q + 1, t1, t0, w0, w1, BsB, BsE, false);
+        stage(q + 2, t2, t1, w1, w0, BsC, BsF, true);
+        stage(q + 3, t0, t2, w0, w1, BsD, BsA, false);
+        stage(q + 4, t1, t0, w1, w0, BsE, BsB, true);
+        stage(q + 5, t2, t1, w0, w1, BsF, BsC, false);
       }
-      if (q < nq) stage(q, t0, t2, w1, w0, BsA, BsD, false);
-      if (q + 1 < nq) stage(q + 1, t1, t0, w0, w1, BsB, BsE, true);
-      if (q + 2 < nq) stage(q + 2, t2, t1, w1, w0, BsC, BsF, false);
-      if (q + 3 < nq) stage(q + 3, t0, t2, w0, w1, BsD, BsA, true);
-      if (q + 4 < nq) stage(q + 4, t1, t0, w1, w0, BsE, BsB, false);
+      if (q < nq) stage(q, t0, t2, w1, w0, BsA, BsD, true);
+      if (q + 1 < nq) stage(q + 1, t1, t0, w0, w1, BsB, BsE, false);
+      if (q + 2 < nq) stage(q + 2, t2, t1, w1, w0, BsC, BsF, true);
+      if (q + 3 < nq) stage(q + 3, t0, t2, w0, w1, BsD, BsA, false);
+      if (q + 4 < nq) stage(q + 4, t1, t0, w1, w0, BsE, BsB, true);
     } else {
       for (; q + 5 < nq; q += 6) {
         stage(q, t0, t2, w1, w0, BsA, BsC, true);
