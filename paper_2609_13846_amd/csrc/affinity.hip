@@ -47,7 +47,8 @@ constexpr int kThreads = 256;
 constexpr int kSliceTokens = 1 << 18;  // tokens per internal slice (size of the 1/r buffer)
 constexpr int kMaxSplits = 128;        // token splits per launch (size of the partials)
 constexpr int kTileTokens = 1 << 15;   // tokens per bf16 slice (size of the tiled token buffer)
-constexpr int kTargetBlocks = 3072;    // aim for this many blocks per launch
+constexpr int kTargetBlocks = 768;     // bf16 kernel: aim for this many blocks per launch
+constexpr int kTargetBlocksF32 = 768;  // fp32 kernel: the same, in blocks of 4 waves
 constexpr size_t kLdsPerCu = 160 * 1024;  // LDS bytes per CU (gfx950)
 
 template <typename T>
@@ -1236,7 +1237,7 @@ dtp_status accumulate(dtp_layer L, const void* x, const void* attn, const void* 
       DTP_CHECK(splits > 0, DTP_ERR_UNSUPPORTED,
                 "affinity kernel: %d groups need more LDS than a CU holds", G);
     } else {
-      splits = (kTargetBlocks / 4 + L->n_tiles - 1) / L->n_tiles;
+      splits = (kTargetBlocksF32 + L->n_tiles - 1) / L->n_tiles;
       splits = std::max(1, std::min(splits, std::min(T, kMaxSplits)));
       AffinityF32Args p;
       p.x = (const float*)xs;
