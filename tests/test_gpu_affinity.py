@@ -82,6 +82,17 @@ def test_affinity_full_qwen_layer_sampled_neurons():
     assert np.all(A > 0)
 
 
+@pytest.mark.parametrize("G", [26, 32])
+def test_affinity_many_tiles_per_block_sampled_neurons(G):
+    """8,192 tokens at G = 26 (six copy buffers) and G = 32 (three): 32 tiles of 256 tokens
+    over 16 token splits, so each block runs two tiles back to back."""
+    wl, w, x, a = case("qwen3-0.6b-layer", 8192, n_q_heads=G, n_kv_groups=G, head_dim=64)
+    announce(f"affinity G={G} T=8192 sampled neurons")
+    A = hp.gpu_affinity(wl, w, x, a)
+    cols = np.r_[0:32, 1500:1532, wl.n_neurons - 32:wl.n_neurons]
+    hp.assert_affinity_close(A[:, cols], oracle(wl, w, x, a, neurons=cols))
+
+
 def test_empty_and_single_token():
     wl, w, x, a = case("qwen3-0.6b-layer", 1)
     announce("affinity T=0 and T=1")
