@@ -21,13 +21,14 @@
 //   fold_kernel           F = W' W_o (MFMA)
 //   down_norm_*_kernel    n_d[k] = ||w^d_k||^2 (row chunks, then their fixed-order sum)
 //   rms_kernel            1/r per token
+//   tile_tokens_kernel    [x | a] rewritten in MFMA fragment order, 1 KB per 32-row k-step
 //   affinity_bf16_kernel  the fused operating point + per-head damage + token reduction
 //   reduce_splits_kernel  deterministic fp64 sum of the per-split partials into A
 // The bf16 weights of a neuron tile form one K-contiguous operand of 128 rows (64 gate,
 // 64 up) and d + H*dh columns: [W' | F_0 | F_1 | ... | F_{H-1}].  The token operand is the
-// matching concatenation [x | a_0 | ... | a_{H-1}] read straight from the caller's x and
-// attn, so the fused kernel is one contraction over d + H*dh with epilogues at the
-// operating-point and head boundaries.
+// matching concatenation [x | a_0 | ... | a_{H-1}] of the caller's x and attn, tiled once
+// per slice so that every fragment load is contiguous; the fused kernel is one
+// contraction over d + H*dh with epilogues at the operating-point and head boundaries.
 // The fp32 path (dtype DTP_F32) runs the same decomposition with plain FMA kernels.
 #include <cmath>
 #include <vector>
@@ -622,8 +623,8 @@ affinity_bf16_kernel(AffinityArgs p) {
   static_assert(kNeurons % kBN == 0, "a block covers whole 64-neuron tiles");
   using WStage = WeightStage<KC, kStageCols, NT>;
   // KC = 64 or 32 with one 64-neuron group: weight stages copied straight into LDS (DmaWeights),
-  // in two separate buffers, so the compiler can tell the reads of one stage from the copy
-  // into the other (one array indexed by the stage parity makes it wait for the copy
+  // each stage's buffer a separate array, so the compiler can tell the reads of one stage
+  // from the copy into another (one array indexed by the stage makes it wait for the copy
   // before every read).  Otherwise through registers into a padded double buffer.
   constexpr bool kDma = (KC == 64 || KC == 32) && kStageCols == 128 && NT == 512;
   // Copied stages rotate through RING buffers: with three, every stage ends at a barrier;
