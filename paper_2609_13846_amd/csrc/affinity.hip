@@ -627,10 +627,12 @@ affinity_bf16_kernel(AffinityArgs p) {
   // from the copy into another (one array indexed by the stage makes it wait for the copy
   // before every read).  Otherwise through registers into a padded double buffer.
   constexpr bool kDma = (KC == 64 || KC == 32) && kStageCols == 128 && NT == 512;
-  // Copied stages rotate through RING buffers: with three, every stage ends at a barrier;
-  // with six, every second one does (stage q+3 is copied during stage q).
-  static_assert(RING == 3 || (RING == 6 && kDma), "three or six copy buffers");
-  constexpr bool kPairs = RING == 6;
+  // Copied stages rotate through RING buffers: with three, every stage ends at a barrier
+  // (stage q+2 is copied during stage q); with six, every second one does (stage q+3
+  // copied); with nine, every third (stage q+4 copied).
+  static_assert(RING == 3 || ((RING == 6 || RING == 9) && kDma), "three, six or nine copy buffers");
+  constexpr bool kPairs = RING >= 6;  // not every stage ends at a barrier
+  constexpr int kLead = RING == 9 ? 4 : RING == 6 ? 3 : 2;  // stages a copy runs ahead
   __shared__ __attribute__((aligned(16))) uint16_t Bs[2][kDma ? 8 : kStageCols * (KC + 8)];
   __shared__ __attribute__((aligned(16))) uint16_t BsA[kDma ? kStageCols * KC : 8];
   __shared__ __attribute__((aligned(16))) uint16_t BsB[kDma ? kStageCols * KC : 8];
@@ -638,6 +640,9 @@ affinity_bf16_kernel(AffinityArgs p) {
   __shared__ __attribute__((aligned(16))) uint16_t BsD[kPairs ? kStageCols * KC : 8];
   __shared__ __attribute__((aligned(16))) uint16_t BsE[kPairs ? kStageCols * KC : 8];
   __shared__ __attribute__((aligned(16))) uint16_t BsF[kPairs ? kStageCols * KC : 8];
+  __shared__ __attribute__((aligned(16))) uint16_t BsG[RING == 9 ? kStageCols * KC : 8];
+  __shared__ __attribute__((aligned(16))) uint16_t BsH[RING == 9 ? kStageCols * KC : 8];
+  __shared__ __attribute__((aligned(16))) uint16_t BsI[RING == 9 ? kStageCols * KC : 8];
   __shared__ __attribute__((aligned(16))) float rv[kRows];  // 1/r of the tile's rows, 0 past T
   __shared__ __attribute__((aligned(16))) float rv2[kRows];  // 1/r' of the rows (down statistic)
   extern __shared__ float red[];  // [WM*WN][G+1][32*NB]
@@ -713,7 +718,8 @@ affinity_bf16_kernel(AffinityArgs p) {
     if constexpr (kDma) {
       dma.copy(w_rsrc, BsA, wave, 0);
       dma.copy(w_rsrc, BsB, wave, min(1, nq - 1) * KC);
-      if constexpr (kPairs) dma.copy(w_rsrc, BsC, wave, min(2, nq - 1) * KC);
+      if constexpr (kLead > 2) dma.copy(w_rsrc, BsC, wave, min(2, nq - 1) * KC);
+      if constexpr (kLead > 3) dma.copy(w_rsrc, BsD, wave, min(3, nq - 1) * KC);
     } else {
       load_weights(w1, w_rsrc, w_off, min(1, nq - 1) * KC);
       store_weights(w0, Bs[0]);
@@ -735,8 +741,10 @@ affinity_bf16_kernel(AffinityArgs p) {
     // buffer of stage q-3, which all waves left before the last barrier, and the barrier
     // after stage 2p waits for the copies of stages 2p+1 and 2p+2.  A head of two stages
     // then ends with no barrier after its epilogue, so one wave's epilogue can run beside
-    // the other wave's next MFMAs.  `sync`: the stage ends at a barrier (with three
-    // buffers, every stage does).
+    // the other wave's next MFMAs.  Nine buffers do the same with windows of three stages
+    // (barriers after stages 3m; stage q+4 copied into the buffer of stage q-5), for
+    // heads of three stages.  `sync`: the stage ends at a barrier (with three buffers,
+    // every stage does).
     auto stage = [&](int q, TokenRows<KC, RB>& cur, TokenRows<KC, RB>& tnew, WStage& wnext,
                      WStage& wnew, uint16_t* bcur, uint16_t* bnxt, bool sync) __attribute__((always_inline)) {
       const int buf = q & 1;
@@ -744,7 +752,7 @@ affinity_bf16_kernel(AffinityArgs p) {
       // counts before each use stay exact instead of falling back to a full drain.
       const int qn = min(q + 2, nq - 1);
       if constexpr (kDma) {
-        dma.copy(w_rsrc, bnxt, wave, min(q + (kPairs ? 3 : 2), nq - 1) * KC);
+        dma.copy(w_rsrc, bnxt, wave, min(q + kLead, nq - 1) * KC);
         // Keep the copy ahead of the token loads: the wait at the end of the stage counts
         // on the loads issued after it.
         __builtin_amdgcn_sched_barrier(0);
@@ -871,7 +879,29 @@ affinity_bf16_kernel(AffinityArgs p) {
     // Unrolled by six so the three token and two weight register sets, and the three or
     // six copy buffers, rotate in place.
     int q = 0;
-    if constexpr (kPairs) {
+    if constexpr (RING == 9) {
+      // Barriers after the stages q = 0 mod 3: with the operating point a multiple of three
+      // stages and three-stage heads, no head epilogue is followed by a barrier.
+      for (; q + 8 < nq; q += 9) {
+        stage(q, t0, t2, w1, w0, BsA, BsE, true);
+        stage(q + 1, t1, t0, w0, w1, BsB, BsF, false);
+        stage(q + 2, t2, t1, w1, w0, BsC, BsG, false);
+        stage(q + 3, t0, t2, w0, w1, BsD, BsH, true);
+        stage(q + 4, t1, t0, w1, w0, BsE, BsI, false);
+        stage(q + 5, t2, t1, w0, w1, BsF, BsA, false);
+        stage(q + 6, t0, t2, w1, w0, BsG, BsB, true);
+        stage(q + 7, t1, t0, w0, w1, BsH, BsC, false);
+        stage(q + 8, t2, t1, w1, w0, BsI, BsD, false);
+      }
+      if (q < nq) stage(q, t0, t2, w1, w0, BsA, BsE, true);
+      if (q + 1 < nq) stage(q + 1, t1, t0, w0, w1, BsB, BsF, false);
+      if (q + 2 < nq) stage(q + 2, t2, t1, w1, w0, BsC, BsG, false);
+      if (q + 3 < nq) stage(q + 3, t0, t2, w0, w1, BsD, BsH, true);
+      if (q + 4 < nq) stage(q + 4, t1, t0, w1, w0, BsE, BsI, false);
+      if (q + 5 < nq) stage(q + 5, t2, t1, w0, w1, BsF, BsA, false);
+      if (q + 6 < nq) stage(q + 6, t0, t2, w1, w0, BsG, BsB, true);
+      if (q + 7 < nq) stage(q + 7, t1, t0, w0, w1, BsH, BsC, false);
+    } else if constexpr (kPairs) {
       for (; q + 5 < nq; q += 6) {
         stage(q, t0, t2, w1, w0, BsA, BsD, true);
         stage(q + 1, t1, t0, w0, w1, BsB, BsE, false);
@@ -954,9 +984,15 @@ int launch_affinity(AffinityArgs p, hipStream_t s) {
 }
 
 // The 64- and 32-deep kernels with six copy buffers where the block fits the LDS with 8 KB
-// to spare (G up to 26 at KC = 64), else with three.
+// to spare (G up to 26 at KC = 64), else with three.  At KC = 32 with heads and operating
+// point in multiples of three stages, nine buffers (72 KB, any G).
 template <int KC, bool ADD>
 int launch_affinity_copied(AffinityArgs p, hipStream_t s) {
+  if constexpr (KC == 32) {
+    if ((p.dh / KC) % 3 == 0 && (p.d / KC) % 3 == 0 &&
+        affinity_lds_fits<KC, 8, 1, 1, 2, true, 4, ADD, 9>(affinity_dynamic_lds<8, 1, 2>(p.G), 8192))
+      return launch_affinity<KC, 8, 1, 1, 2, true, 4, ADD, 9>(p, s);
+  }
   if (affinity_lds_fits<KC, 8, 1, 1, 2, true, 4, ADD, 6>(affinity_dynamic_lds<8, 1, 2>(p.G), 8192))
     return launch_affinity<KC, 8, 1, 1, 2, true, 4, ADD, 6>(p, s);
   return launch_affinity<KC, 8, 1, 1, 2, true, 4, ADD, 3>(p, s);

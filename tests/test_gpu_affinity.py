@@ -53,6 +53,9 @@ def oracle(wl, w, x, a, neurons=None):
     # an odd number of stages (three), so the last one ends an unfinished pair of stages
     ("qwen3-0.6b-layer", 600, dict(d_model=128, n_q_heads=1, n_kv_groups=1, head_dim=64, n_neurons=128)),
     ("danube3-500m", 300, dict(d_model=64, n_q_heads=1, n_kv_groups=1, head_dim=32, n_neurons=64)),
+    # three-stage heads (nine copy buffers): six stages, fewer than the ring, and nine
+    ("danube3-500m", 300, dict(d_model=96, n_q_heads=1, n_kv_groups=1, head_dim=96, n_neurons=64)),
+    ("danube3-500m", 600, dict(d_model=96, n_q_heads=2, n_kv_groups=1, head_dim=96, n_neurons=128)),
 ])
 def test_affinity_matches_oracle(name, T, shape):
     wl, w, x, a = case(name, T, **shape)
@@ -90,6 +93,15 @@ def test_affinity_many_tiles_per_block_sampled_neurons(G):
     announce(f"affinity G={G} T=8192 sampled neurons")
     A = hp.gpu_affinity(wl, w, x, a)
     cols = np.r_[0:32, 1500:1532, wl.n_neurons - 32:wl.n_neurons]
+    hp.assert_affinity_close(A[:, cols], oracle(wl, w, x, a, neurons=cols))
+
+
+def test_affinity_danube_many_tiles_per_block_sampled_neurons():
+    """8,192 Danube-shaped tokens (nine copy buffers): 32 tiles over 12 token splits."""
+    wl, w, x, a = case("danube3-500m", 8192)
+    announce("affinity danube3-500m T=8192 sampled neurons")
+    A = hp.gpu_affinity(wl, w, x, a)
+    cols = np.r_[0:32, 2000:2032, wl.n_neurons - 32:wl.n_neurons]
     hp.assert_affinity_close(A[:, cols], oracle(wl, w, x, a, neurons=cols))
 
 
