@@ -358,3 +358,152 @@ def test_unlabelled_partition_counts():
     for G, L in [(8, 4), (8, 2), (6, 3), (4, 2)]:
         n = math.factorial(G) // (math.factorial(G // L) ** L * math.factorial(L))
         assert len(lay.unlabelled_partitions(G, L)) == n
+
+
+# ----------------------------------------------------------------------------- chain coupling
+# Eq. (objective) read off the paper term by term, written as plain loops that share nothing
+# with the oracle: up edge i counts S_up_i[g, k] when KV group g of layer i and neuron k of
+# layer i share a device; down edge i counts S_down_i[k, g] when neuron k of layer i and KV
+# group g of layer i + 1 share one.  The block steps of the optimiser (Section 3,
+# "Optimiser": M_kl given h_i and h_{i+1}; the head step given nu_{i-1} and nu_i) are then
+# pinned by brute force over that J alone, on chains whose neighbouring layouts differ, so a
+# term keyed to the wrong layer changes the answer.
+def chain_J(Qu, Qd, hs, nus):
+    N = len(Qu)
+    J = 0
+    for i in range(N):
+        G, I = Qu[i].shape
+        for g in range(G):
+            for k in range(I):
+                if hs[i][g] == nus[i][k]:
+                    J += int(Qu[i][g, k])
+    if Qd is not None:
+        for i in range(N - 1):
+            I, G = Qd[i].shape
+            for k in range(I):
+                for g in range(G):
+                    if nus[i][k] == hs[i + 1][g]:
+                        J += int(Qd[i][k, g])
+    return J
+
+
+def _distinct_layouts(rng, N, G, I, L):
+    """Balanced layouts in which no two neighbouring layers share h or nu."""
+    parts = lay.partitions(G, L)
+    while True:
+        hs = [np.array(parts[rng.integers(len(parts))]) for _ in range(N)]
+        nus = [rng.permutation(np.arange(I) // (I // L)) for _ in range(N)]
+        if all(not np.array_equal(hs[i], hs[i + 1]) and not np.array_equal(nus[i], nus[i + 1])
+               for i in range(N - 1)):
+            return hs, nus
+
+
+@pytest.mark.parametrize("N,G,I,L", [(2, 4, 8, 2), (3, 4, 8, 2), (3, 8, 16, 4)])
+def test_objective_equals_explicit_chain_sum(N, G, I, L):
+    rng = np.random.default_rng(40 + N + L)
+    Qu = [rand_Q(rng, (G, I)) for _ in range(N)]
+    Qd = [rand_Q(rng, (I, G)) for _ in range(N - 1)]
+    for _ in range(20):
+        hs, nus = _distinct_layouts(rng, N, G, I, L)
+        assert lay.objective(Qu, Qd, hs, nus) == chain_J(Qu, Qd, hs, nus)
+        assert lay.objective(Qu, None, hs, nus) == chain_J(Qu, None, hs, nus)
+
+
+def test_single_down_entry_counts_with_the_next_layers_group():
+    """One unit of down mass between neuron k of layer 0 and KV group g of layer 1 counts
+    exactly when nu_0(k) == h_1(g), whatever h_0 and nu_1 are."""
+    G, I, L = 4, 4, 2
+    Qu = [np.zeros((G, I), np.int64) for _ in range(2)]
+    k, g = 1, 2
+    Qd = [np.zeros((I, G), np.int64)]
+    Qd[0][k, g] = 1
+    for h0 in lay.partitions(G, L):
+        for h1 in lay.partitions(G, L):
+            for nu0 in ([0, 0, 1, 1], [1, 1, 0, 0], [0, 1, 0, 1]):
+                nus = [np.array(nu0), np.array([0, 1, 1, 0])]
+                want = int(nu0[k] == h1[g])
+                assert lay.objective(Qu, Qd, [np.array(h0), np.array(h1)], nus) == want
+
+
+def _all_balanced(n, L):
+    return [np.array(v) for v in itertools.product(range(L), repeat=n)
+            if all(v.count(l) == n // L for l in range(L))]
+
+
+@pytest.mark.parametrize("N,G,I,L,seed", [(2, 4, 8, 2, 50), (3, 4, 8, 2, 51), (3, 4, 8, 4, 52)])
+def test_neuron_block_is_the_brute_force_optimum_of_the_chain(N, G, I, L, seed):
+    """Given every h and the other layers' nu, the oracle's neuron step for layer i
+    (M_kl from h_i and h_{i+1}) attains the maximum of J over all balanced nu_i."""
+    rng = np.random.default_rng(seed)
+    nus_all = _all_balanced(I, L)
+    for _ in range(4):
+        Qu = [rand_Q(rng, (G, I)) for _ in range(N)]
+        Qd = [rand_Q(rng, (I, G)) for _ in range(N - 1)]
+        hs, nus = _distinct_layouts(rng, N, G, I, L)
+        for i in range(N):
+            down = Qd[i] if i + 1 < N else None
+            M = lay.neuron_gain(Qu[i], hs[i], L, down, hs[i + 1] if down is not None else None)
+            nu_i, _ = lay.balanced_assign(M)
+
+            def J_with(v):
+                trial = list(nus)
+                trial[i] = v
+                return chain_J(Qu, Qd, hs, trial)
+            best = max(J_with(v) for v in nus_all)
+            assert J_with(nu_i) == best, f"layer {i}"
+
+
+@pytest.mark.parametrize("N,G,I,L,seed", [(2, 4, 8, 2, 60), (3, 4, 8, 2, 61), (3, 8, 8, 4, 62)])
+def test_head_block_is_the_brute_force_optimum_of_the_chain(N, G, I, L, seed):
+    """Given every nu and the other layers' h, the oracle's head step for layer i (C from
+    nu_i and nu_{i-1}) picks the lowest-rank partition among those maximising J."""
+    rng = np.random.default_rng(seed)
+    parts = lay.partitions(G, L)
+    for _ in range(4):
+        Qu = [rand_Q(rng, (G, I)) for _ in range(N)]
+        Qd = [rand_Q(rng, (I, G)) for _ in range(N - 1)]
+        hs, nus = _distinct_layouts(rng, N, G, I, L)
+        for i in range(N):
+            prev = Qd[i - 1] if i > 0 else None
+            C = lay.head_gain(Qu[i], nus[i], L, prev, nus[i - 1] if prev is not None else None)
+            pick = lay.best_partition(lay.partition_scores(C, parts))
+
+            def J_with(h):
+                trial = list(hs)
+                trial[i] = np.array(h)
+                return chain_J(Qu, Qd, trial, nus)
+            Js = [J_with(h) for h in parts]
+            assert pick == int(np.argmax(Js)), f"layer {i}"
+
+
+def test_ascent_chain_blocks_by_brute_force_at_termination():
+    """The ascent's final layout of a 3-layer chain: no balanced nu_i or h_i alone raises
+    the explicit J (generic data, so the last sweep changed nothing)."""
+    rng = np.random.default_rng(70)
+    N, G, I, L = 3, 4, 8, 2
+    Qu = [rand_Q(rng, (G, I)) for _ in range(N)]
+    Qd = [rand_Q(rng, (I, G)) for _ in range(N - 1)]
+    hs, nus, J, _ = lay.coordinate_ascent(Qu, Qd, L)
+    hs = [np.array(h) for h in hs]
+    assert J == chain_J(Qu, Qd, hs, nus)
+    for i in range(N):
+        for v in _all_balanced(I, L):
+            trial = list(nus)
+            trial[i] = v
+            assert chain_J(Qu, Qd, hs, trial) <= J
+        for h in lay.partitions(G, L):
+            trial = list(hs)
+            trial[i] = np.array(h)
+            assert chain_J(Qu, Qd, trial, nus) <= J
+
+
+def test_two_layer_chain_ascent_below_brute_force_optimum_of_explicit_J():
+    rng = np.random.default_rng(71)
+    G, I, L = 4, 4, 2
+    hs_all, nus_all = all_layouts(G, I, L)
+    Qu = [rand_Q(rng, (G, I)) for _ in range(2)]
+    Qd = [rand_Q(rng, (I, G))]
+    _, _, J, _ = lay.coordinate_ascent(Qu, Qd, L)
+    Jstar = max(chain_J(Qu, Qd, [np.array(h0), np.array(h1)], [n0, n1])
+                for h0 in hs_all for h1 in hs_all for n0 in nus_all for n1 in nus_all)
+    assert 0 < J <= Jstar

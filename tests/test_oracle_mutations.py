@@ -230,3 +230,40 @@ def test_offsets_moving_the_wrong_way_are_caught(monkeypatch):
     M[:, 0] = 10          # every neuron prefers device 0: the offsets must push them away
     lam, _ = da.dual_offsets(M)
     assert lam[0] < 0     # wrong direction: device 0 got cheaper
+
+
+# ---- chain coupling of eq. (objective) and of the two block steps
+def test_neuron_gain_down_term_keyed_to_own_heads_is_caught(monkeypatch):
+    orig = lay.neuron_gain
+
+    def bad(Q_up, h, L, Q_down=None, h_next=None):   # down edge against h_i, not h_{i+1}
+        return orig(Q_up, h, L, Q_down, h if Q_down is not None else None)
+    monkeypatch.setattr(lay, "neuron_gain", bad)
+    with pytest.raises(AssertionError):
+        pl.test_neuron_block_is_the_brute_force_optimum_of_the_chain(3, 4, 8, 2, 51)
+
+
+def test_head_gain_down_term_keyed_to_own_neurons_is_caught(monkeypatch):
+    orig = lay.head_gain
+
+    def bad(Q_up, nu, L, Q_down_prev=None, nu_prev=None):   # nu_i, not nu_{i-1}
+        return orig(Q_up, nu, L, Q_down_prev, nu if Q_down_prev is not None else None)
+    monkeypatch.setattr(lay, "head_gain", bad)
+    with pytest.raises(AssertionError):
+        pl.test_head_block_is_the_brute_force_optimum_of_the_chain(3, 4, 8, 2, 61)
+
+
+def test_objective_down_edge_keyed_to_own_heads_is_caught(monkeypatch):
+    def bad(Q_up, Q_down, hs, nus):
+        J = 0
+        for i in range(len(Q_up)):
+            h, nu = np.asarray(hs[i]), np.asarray(nus[i])
+            J += int(Q_up[i][h[:, None] == nu[None, :]].sum())
+            if Q_down is not None and i + 1 < len(Q_up):
+                J += int(Q_down[i][nu[:, None] == h[None, :]].sum())   # h_i, not h_{i+1}
+        return J
+    monkeypatch.setattr(lay, "objective", bad)
+    with pytest.raises(AssertionError):
+        pl.test_objective_equals_explicit_chain_sum(3, 4, 8, 2)
+    with pytest.raises(AssertionError):
+        pl.test_single_down_entry_counts_with_the_next_layers_group()
