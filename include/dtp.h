@@ -16,6 +16,11 @@
  *   - "dev" pointers are device memory of the current HIP device; "host" pointers are
  *     ordinary host memory.  The caller owns every buffer it passes; the library keeps
  *     no caller pointer after a call returns.  Device tensors are dense row-major.
+ *   - Every dev argument is checked before any work is enqueued: it must be memory of the
+ *     current device (hipPointerGetAttributes) whose allocation holds every byte the call
+ *     reads or writes from that address on (hipMemGetAddressRange); otherwise the call
+ *     returns DTP_ERR_INVALID_ARG.  Host arrays cannot be checked: their sizes are the
+ *     caller's responsibility.
  *   - `stream` is a hipStream_t (NULL = the default stream).  GPU work is enqueued on it
  *     asynchronously; functions that return host results synchronise that stream first.
  *   - Weights use the PyTorch nn.Linear layout [out_features, in_features].
@@ -42,7 +47,7 @@ typedef enum {
 typedef enum { DTP_BF16 = 0, DTP_F32 = 1 } dtp_dtype;
 
 /* Shapes of one decoder layer.  Query head h belongs to KV group h / (H/G).
- * Constraints: all sizes > 0; H % G == 0; G <= 32; head_dim % 16 == 0; d_model % 8 == 0;
+ * Constraints: all sizes > 0; H % G == 0; G <= 32; head_dim % 16 == 0; d_model % 16 == 0;
  * rms_eps >= 0; dtype is DTP_BF16 (MFMA path) or DTP_F32 (reference-precision path). */
 typedef struct {
   int32_t d_model;      /* d */
@@ -88,6 +93,13 @@ dtp_status dtp_layer_set_weights(dtp_layer layer, const void* w_o, const void* g
 dtp_status dtp_affinity_accumulate(dtp_layer layer, const void* x, const void* attn,
                                    int64_t n_tokens, float* A, void* stream);
 
+/* The simpler ADD score of Section 3 ("Affinity scores") over the same token stream:
+ *   A[g, k] += sum_t sum_{h in g} (p_h . w^g_k)^2 + (p_h . w^u_k)^2,
+ * which ignores the operating point of the nonlinearity and the neuron's write (no
+ * ||w^d_k||^2 factor).  Arguments as for dtp_affinity_accumulate. */
+dtp_status dtp_affinity_accumulate_add(dtp_layer layer, const void* x, const void* attn,
+                                       int64_t n_tokens, float* A, void* stream);
+
 /* The same accumulation of A, plus the token statistic of the down edge (Section 3,
  * "Affinity scores", down edge) in the same pass:
  *   s_down[k] += sum_t alpha_k(t)^2 / r'_t^2,  alpha_k = silu(g_k) u_k,
@@ -97,13 +109,6 @@ dtp_status dtp_affinity_accumulate(dtp_layer layer, const void* x, const void* a
  *   x_next dev [n_tokens, d]  layer dtype, 16-byte aligned
  *   s_down dev [I] float       accumulated in place (+=); deterministic for fixed shapes
  * x_next and s_down are both required (DTP_ERR_INVALID_ARG otherwise). */
-/* The simpler ADD score of Section 3 ("Affinity scores") over the same token stream:
- *   A[g, k] += sum_t sum_{h in g} (p_h . w^g_k)^2 + (p_h . w^u_k)^2,
- * which ignores the operating point of the nonlinearity and the neuron's write (no
- * ||w^d_k||^2 factor).  Arguments as for dtp_affinity_accumulate. */
-dtp_status dtp_affinity_accumulate_add(dtp_layer layer, const void* x, const void* attn,
-                                       int64_t n_tokens, float* A, void* stream);
-
 dtp_status dtp_affinity_accumulate_down(dtp_layer layer, const void* x, const void* attn,
                                         const void* x_next, float rms_eps_next,
                                         int64_t n_tokens, float* A, float* s_down,
@@ -219,8 +224,8 @@ dtp_status dtp_balanced_assign_dual_ascent(int32_t G, int32_t I, int32_t L, cons
 /* Options of the coordinate ascent; NULL means the defaults
  * {max_sweeps = 64, freeze_heads = 0, freeze_neurons = 0, minimise = 0, layer_mask = NULL,
  *  dual_ascent_neurons = 0}.
- * freeze_*: keep that block at its contiguous start.  layer_mask (host [N] or NULL): a zero
- * entry keeps layer i contiguous.  minimise: minimise J instead (anti-optimised layouts).
+ * freeze_*: keep that block at its contiguous start.  layer_mask (host, exactly N entries,
+ * or NULL): a zero entry keeps layer i contiguous.  minimise: minimise J instead (anti-optimised layouts).
  * dual_ascent_neurons: solve the neuron step with the paper's approximate method
  * (dtp_balanced_assign_dual_ascent) instead of exactly. */
 typedef struct {
@@ -275,9 +280,9 @@ dtp_status dtp_layer_optimum(int32_t G, int32_t I, int32_t L, const int64_t* Q_u
                              int32_t* nu, int64_t* J_fixed);
 
 /* ---------------------------------------------------------------------------------------
- * Applying a layout (Section 3, "Problem").  Device l's shard holds the KV groups and
- * neurons that (h, nu) put on l, in increasing original index; shards follow in device
- * order.  The permuted layer computes the same function (rotary embeddings, per-head norms
+ * Applying a layout (Section 3, "The layout as a free variable").  Device l's shard holds
+ * the KV groups and neurons that (h, nu) put on l, in increasing original index; shards
+ * follow in device order.  The permuted layer computes the same function (rotary embeddings, per-head norms
  * and SwiGLU act per head or per neuron).
  * ------------------------------------------------------------------------------------- */
 
@@ -294,7 +299,8 @@ dtp_status dtp_layout_orders(int32_t G, int32_t I, int32_t L, const int32_t* h, 
  * w_up and columns of w_down move with the neurons.  Gains and per-head norm weights are
  * unchanged and not touched.  h host [G], nu host [I].  dst must not alias src.
  * Bit-exact data movement; a [G + I] int32 scratch comes from the stream-ordered
- * allocator and is returned before exit. */
+ * allocator and is returned before exit.  Synchronises `stream` (the order table is
+ * uploaded from host memory that the call owns). */
 dtp_status dtp_apply_layout(const dtp_layer_desc* desc, int32_t L, const int32_t* h,
                             const int32_t* nu, const void* const* src, void* const* dst,
                             void* stream);

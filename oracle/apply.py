@@ -3,12 +3,14 @@
 Only ``tests/``, ``__graft_entry__.smoke()`` and ``bench.py``'s ``cpu_baseline`` leg may
 import this module.  It shares no code with the HIP library.
 
-Section 3 ("Problem"): a pair (h_i, nu_i) is realised by permuting the rows of the query,
-key and value projections by KV group (each group's query heads travel with its KV head)
-and the columns of the output projection identically, and the rows of the gate and up
-projections and the columns of the down projection identically, then slicing contiguous
-shards.  The dense function is unchanged because rotary embeddings, per-head norms and
-the SwiGLU nonlinearity act per head or per neuron.
+Section 3, "The layout as a free variable": the layout (h_i, nu_i) of a layer becomes an
+ordering of its KV groups and of its neurons (device 0's in increasing original index,
+then device 1's, ...).  Every weight indexed by a group (the query rows of its query
+heads, its key and value rows, the matching output-projection columns) and every weight
+indexed by a neuron (gate and up rows, down-projection columns) is reordered with it, so
+each device's shard is a contiguous slice.  Rotary embeddings, per-head norms and the
+SwiGLU product work head by head or neuron by neuron, which is why the reordered layer
+computes the same function.
 
 Reading (listed in the design notes): device l's shard holds its groups and neurons in
 increasing original index, and the shards follow each other in device order.

@@ -27,6 +27,35 @@ dtp_status fail(dtp_status s, const char* fmt, ...) {
 
 void clear_error() { g_last_error[0] = '\0'; }
 
+dtp_status check_dev_buffer(const void* p, size_t bytes, const char* what, bool optional) {
+  if (p == nullptr) {
+    DTP_CHECK(optional, DTP_ERR_INVALID_ARG, "%s is NULL", what);
+    return DTP_OK;
+  }
+  int dev = -1;
+  DTP_HIP(hipGetDevice(&dev));
+  hipPointerAttribute_t a{};
+  if (hipPointerGetAttributes(&a, p) != hipSuccess) {
+    (void)hipGetLastError();  // keep the failed query out of later launch checks
+    return fail(DTP_ERR_INVALID_ARG, "%s (%p) is not device memory", what, p);
+  }
+  DTP_CHECK(a.type == hipMemoryTypeDevice || a.type == hipMemoryTypeManaged, DTP_ERR_INVALID_ARG,
+            "%s (%p) is not device memory (HIP memory type %d)", what, p, (int)a.type);
+  DTP_CHECK(a.device == dev, DTP_ERR_INVALID_ARG, "%s (%p) is memory of device %d, not of the current device %d",
+            what, p, a.device, dev);
+  hipDeviceptr_t base = nullptr;
+  size_t size = 0;
+  if (hipMemGetAddressRange(&base, &size, const_cast<void*>(p)) != hipSuccess) {
+    (void)hipGetLastError();
+    return fail(DTP_ERR_INVALID_ARG, "%s (%p): no device allocation contains it", what, p);
+  }
+  const size_t off = (size_t)((const char*)p - (const char*)base);
+  DTP_CHECK(off <= size && bytes <= size - off, DTP_ERR_INVALID_ARG,
+            "%s (%p) has %zu bytes left in its allocation, the call reads or writes %zu", what, p,
+            off <= size ? size - off : (size_t)0, bytes);
+  return DTP_OK;
+}
+
 namespace {
 
 // M[k][l] = sum_{g: h(g)=l} Q_up[g][k] + sum_{g: h_next(g)=l} Q_down[k][g], negated when
@@ -193,6 +222,10 @@ dtp_status dtp_encode_affinity_device(const float* A, int64_t n, int64_t* Q, voi
   DTP_CHECK(A != nullptr && Q != nullptr, DTP_ERR_INVALID_ARG, "A or Q is NULL");
   DTP_CHECK(n >= 1 && n <= (int64_t(1) << 30), DTP_ERR_INVALID_ARG,
             "n=%lld outside [1, 2^30]", (long long)n);
+  dtp_status st0;
+  if ((st0 = check_dev_buffer(A, sizeof(float) * (size_t)n, "A")) != DTP_OK ||
+      (st0 = check_dev_buffer(Q, sizeof(int64_t) * (size_t)n, "Q")) != DTP_OK)
+    return st0;
   hipStream_t s = (hipStream_t)stream;
   DevBuf stats_dev(s);
   DTP_HIP(stream_alloc(&stats_dev.p, sizeof(EncodeStats), s));
@@ -257,6 +290,12 @@ dtp_status dtp_partition_scores(int32_t G, int32_t I, int32_t L, const int64_t* 
   const int64_t P = count_partitions(G, L);
   DTP_CHECK(P > 0 && P <= kMaxPartitions, DTP_ERR_UNSUPPORTED,
             "%lld partitions exceed the limit of %lld", (long long)P, (long long)kMaxPartitions);
+  if ((st = check_dev_buffer(Q_up, sizeof(int64_t) * (size_t)G * I, "Q_up")) != DTP_OK ||
+      (st = check_dev_buffer(nu, sizeof(int32_t) * (size_t)I, "nu")) != DTP_OK ||
+      (st = check_dev_buffer(Q_down_prev, sizeof(int64_t) * (size_t)I * G, "Q_down_prev", true)) != DTP_OK ||
+      (st = check_dev_buffer(nu_prev, sizeof(int32_t) * (size_t)I, "nu_prev", true)) != DTP_OK ||
+      (st = check_dev_buffer(scores, sizeof(int64_t) * (size_t)P, "scores")) != DTP_OK)
+    return st;
   hipStream_t s = (hipStream_t)stream;
   // A two-layer view: layer 0 is empty padding so that layer 1 reads Q_down_prev / nu_prev
   // as its incoming down edge.  Without a down edge one layer suffices.
@@ -321,9 +360,12 @@ dtp_status dtp_coordinate_ascent(int32_t N, int32_t G, int32_t I, int32_t L, con
   const int64_t P = count_partitions(G, L);
   DTP_CHECK(P > 0 && P <= kMaxPartitions, DTP_ERR_UNSUPPORTED, "too many partitions (%lld)",
             (long long)P);
-  hipStream_t s = (hipStream_t)stream;
   const bool has_down = A_down != nullptr;
   const size_t nup = (size_t)N * G * I, ndown = has_down ? (size_t)(N - 1) * I * G : 0;
+  if ((st = check_dev_buffer(A_up, sizeof(float) * nup, "A_up")) != DTP_OK ||
+      (st = check_dev_buffer(A_down, sizeof(float) * ndown, "A_down", true)) != DTP_OK)
+    return st;
+  hipStream_t s = (hipStream_t)stream;
 
   // Unit-mass codes of every matrix, computed on the device where the head step reads
   // them; the host copy feeds the neuron step and J.  Layout of the scratch block:

@@ -1197,6 +1197,13 @@ dtp_status accumulate(dtp_layer L, const void* x, const void* attn, const void* 
   const int H = d.n_q_heads, dh = d.head_dim, HD = H * dh, G = d.n_kv_groups;
   const int I = d.n_neurons, dm = d.d_model;
   const size_t esz = d.dtype == DTP_BF16 ? 2 : 4;
+  const size_t nt = (size_t)n_tokens;
+  if ((st = check_dev_buffer(x, esz * nt * dm, "x")) != DTP_OK ||
+      (st = check_dev_buffer(attn, esz * nt * HD, "attn")) != DTP_OK ||
+      (st = check_dev_buffer(A, sizeof(float) * (size_t)G * I, "A")) != DTP_OK ||
+      (st = check_dev_buffer(x_next, esz * nt * dm, "x_next", true)) != DTP_OK ||
+      (st = check_dev_buffer(s_down, sizeof(float) * (size_t)I, "s_down", true)) != DTP_OK)
+    return st;
   // Tokens per slice: the 1/r buffer size, and element offsets of a slice below 2^30.
   const int64_t width = std::max(dm, HD);
   int64_t slice = std::max<int64_t>(256, std::min<int64_t>(kSliceTokens, ((int64_t)1 << 30) / width) / 256 * 256);
@@ -1389,6 +1396,15 @@ dtp_status dtp_layer_set_weights(dtp_layer L, const void* w_o, const void* gamma
   const dtp_layer_desc& d = L->desc;
   const int H = d.n_q_heads, dh = d.head_dim, HD = H * dh, I = d.n_neurons, dm = d.d_model;
   const int64_t n = (int64_t)L->n_tiles * kCols * dm;
+  {
+    const size_t esz = d.dtype == DTP_BF16 ? 2 : 4;
+    const void* ptrs[5] = {w_o, gamma, w_gate, w_up, w_down};
+    const size_t elems[5] = {(size_t)dm * HD, (size_t)dm, (size_t)I * dm, (size_t)I * dm,
+                             (size_t)dm * I};
+    const char* names[5] = {"w_o", "gamma", "w_gate", "w_up", "w_down"};
+    for (int i = 0; i < 5; ++i)
+      if ((st = check_dev_buffer(ptrs[i], esz * elems[i], names[i])) != DTP_OK) return st;
+  }
   if (d.dtype == DTP_BF16) {
     if (aligned16(w_gate) && aligned16(w_up) && aligned16(gamma))
       prep_gate_up_bf16x8_kernel<<<grid_for(n / 8, 256), 256, 0, s>>>(

@@ -1,9 +1,15 @@
-// Applying a layout to a decoder layer's weights (Section 3, "Problem"): a pair (h, nu) is
-// realised by permuting the rows of the q/k/v projections by KV group (each group's query
-// heads travel with it) and the columns of the output projection identically, and the
-// rows of the gate and up projections and the columns of the down projection identically;
-// device l's shard is then a contiguous slice.  Device l holds its groups and neurons in
-// increasing original index, shards in device order.
+// Applying a layout to a decoder layer's weights (Section 3, "The layout as a free
+// variable").  Let group_order[p] be the original KV group placed at new position p and
+// neuron_order[p] the original neuron at new position p, where each list runs through
+// device 0's members in increasing original index, then device 1's, and so on.  With
+// hpg = H/G query heads per group, the permuted weights are
+//   w_q     row block p      (hpg*dh rows)  <- row block group_order[p]
+//   w_k,w_v row block p      (dh rows)      <- row block group_order[p]
+//   w_o     column block p   (hpg*dh cols)  <- column block group_order[p]
+//   w_gate, w_up  row p      <- row neuron_order[p]
+//   w_down  column p         <- column neuron_order[p]
+// so device l's shard is one contiguous range of groups and of neurons.  Gains and
+// per-head norm weights do not move.
 //
 // Kernels (pure data movement, bit-exact):
 //   permute_rows_kernel  out row r = in row of block order[r / block] (16-byte vectors)
@@ -110,6 +116,19 @@ dtp_status dtp_apply_layout(const dtp_layer_desc* desc, int32_t L, const int32_t
   dtp_status st = check_assignment(h, G, L, "h");
   if (st != DTP_OK) return st;
   if ((st = check_assignment(nu, I, L, "nu")) != DTP_OK) return st;
+  {
+    const size_t hd = (size_t)H * dh, gd = (size_t)G * dh;
+    const size_t elems[7] = {hd * dm, gd * dm, gd * dm, (size_t)dm * hd, (size_t)I * dm,
+                             (size_t)I * dm, (size_t)dm * I};
+    const char* src_names[7] = {"src w_q", "src w_k", "src w_v", "src w_o", "src w_gate",
+                                "src w_up", "src w_down"};
+    const char* dst_names[7] = {"dst w_q", "dst w_k", "dst w_v", "dst w_o", "dst w_gate",
+                                "dst w_up", "dst w_down"};
+    for (int i = 0; i < 7; ++i) {
+      if ((st = check_dev_buffer(src[i], esz * elems[i], src_names[i])) != DTP_OK) return st;
+      if ((st = check_dev_buffer(dst[i], esz * elems[i], dst_names[i])) != DTP_OK) return st;
+    }
+  }
   std::vector<int32_t> ord(G + I);
   orders(G, I, L, h, nu, ord.data(), ord.data() + G);
   hipStream_t s = (hipStream_t)stream;
@@ -146,6 +165,8 @@ dtp_status dtp_apply_layout(const dtp_layer_desc* desc, int32_t L, const int32_t
   const hipError_t ef = hipFreeAsync(dord, s);
   DTP_HIP(e);
   DTP_HIP(ef);
+  // The order upload reads `ord`, which dies on return.
+  DTP_HIP(hipStreamSynchronize(s));
   return DTP_OK;
 }
 

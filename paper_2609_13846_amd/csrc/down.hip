@@ -170,6 +170,18 @@ dtp_status dtp_down_weights(int32_t d_model, int32_t n_neurons, int32_t n_q_head
   hipStream_t s = (hipStream_t)stream;
   const int hpg = n_q_heads / n_kv_groups;
   const int64_t GI = (int64_t)n_kv_groups * n_neurons;
+  {
+    const size_t esz = dtype == DTP_BF16 ? 2 : 4, dm = (size_t)d_model;
+    const size_t gd = (size_t)n_kv_groups * head_dim;
+    dtp_status st;
+    if ((st = check_dev_buffer(w_q, esz * n_q_heads * head_dim * dm, "w_q")) != DTP_OK ||
+        (st = check_dev_buffer(w_k, esz * gd * dm, "w_k")) != DTP_OK ||
+        (st = check_dev_buffer(w_v, esz * gd * dm, "w_v")) != DTP_OK ||
+        (st = check_dev_buffer(gamma_next, esz * dm, "gamma_next")) != DTP_OK ||
+        (st = check_dev_buffer(w_down, esz * dm * n_neurons, "w_down")) != DTP_OK ||
+        (st = check_dev_buffer(B, sizeof(float) * (size_t)GI, "B")) != DTP_OK)
+      return st;
+  }
   if (dtype == DTP_F32) {
     DTP_CHECK(d_model % 4 == 0, DTP_ERR_INVALID_ARG, "d_model=%d is not a multiple of 4", d_model);
     down_weight_f32_kernel<<<blocks_for(GI, 256), 256, 0, s>>>(
@@ -210,6 +222,11 @@ dtp_status dtp_down_affinity(int32_t n_neurons, int32_t n_kv_groups, const float
   DTP_CHECK(s_down && B && A_down, DTP_ERR_INVALID_ARG, "s_down, B or A_down is NULL");
   hipStream_t s = (hipStream_t)stream;
   const int64_t n = (int64_t)n_neurons * n_kv_groups;
+  dtp_status st;
+  if ((st = check_dev_buffer(s_down, sizeof(float) * (size_t)n_neurons, "s_down")) != DTP_OK ||
+      (st = check_dev_buffer(B, sizeof(float) * (size_t)n, "B")) != DTP_OK ||
+      (st = check_dev_buffer(A_down, sizeof(float) * (size_t)n, "A_down")) != DTP_OK)
+    return st;
   down_combine_kernel<<<blocks_for(n, 256), 256, 0, s>>>(s_down, B, n_neurons, n_kv_groups, A_down);
   DTP_HIP(hipGetLastError());
   return DTP_OK;

@@ -15,6 +15,13 @@ namespace dtp {
 dtp_status fail(dtp_status s, const char* fmt, ...) __attribute__((format(printf, 2, 3)));
 void clear_error();
 
+// A caller's device buffer: `p` must be memory of the current HIP device whose allocation
+// holds at least `bytes` from `p` on.  A host pointer, another device's memory or a short
+// allocation would make a kernel read or write outside what the caller owns, so every
+// entry point checks its device arguments this way before enqueueing work.  NULL is
+// accepted when `optional` (the argument is then unused).
+dtp_status check_dev_buffer(const void* p, size_t bytes, const char* what, bool optional = false);
+
 #define DTP_HIP(call)                                                                 \
   do {                                                                                \
     hipError_t e_ = (call);                                                           \

@@ -126,6 +126,43 @@ def _ptr(x):
     raise TypeError(f"cannot pass {type(x)!r} as a pointer")
 
 
+def _dev(t, name, dtypes, numel, optional=False):
+    """Address of a device argument after checking it: a contiguous torch tensor on the
+    GPU, of one of ``dtypes`` (torch dtype names), with at least ``numel`` elements.  A
+    plain int is taken as a raw device address (the library still checks that it is
+    device memory large enough for the call)."""
+    if t is None:
+        if optional:
+            return None
+        raise ValueError(f"{name} is required")
+    if isinstance(t, int):
+        return t
+    import torch
+    if not isinstance(t, torch.Tensor):
+        raise TypeError(f"{name} must be a torch tensor on the GPU, not {type(t).__name__}")
+    if not t.is_cuda:
+        raise ValueError(f"{name} must be on the GPU (got a tensor on {t.device})")
+    if str(t.dtype).replace("torch.", "") not in dtypes:
+        raise TypeError(f"{name} must have dtype {' or '.join(dtypes)}, not {t.dtype}")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    if t.numel() < numel:
+        raise ValueError(f"{name} has {t.numel()} elements, the call needs {numel}")
+    return t.data_ptr()
+
+
+def _act_dtypes(dtype):
+    return ("bfloat16",) if dtype == DTP_BF16 else ("float32",)
+
+
+def _host(a, name, dtype, n):
+    """A host array argument of exactly n elements (converted to ``dtype``)."""
+    a = np.ascontiguousarray(a, dtype=dtype)
+    if a.size != n:
+        raise ValueError(f"{name} has {a.size} elements, expected {n}")
+    return a
+
+
 def _stream(stream):
     if stream is not None:
         return stream if isinstance(stream, int) else stream.cuda_stream
@@ -136,49 +173,80 @@ def _stream(stream):
 
 
 # ----------------------------------------------------------------------------- affinity
+# Shapes of the layers created through this module, by handle: what each wrapper checks
+# its device arguments against.
+_LAYERS = {}
+
+
 def dtp_layer_create(d_model, n_neurons, n_q_heads, n_kv_groups, head_dim, rms_eps, dtype):
     desc = dtp_layer_desc(d_model, n_neurons, n_q_heads, n_kv_groups, head_dim, rms_eps, dtype)
     h = _P()
     _check(lib().dtp_layer_create(ctypes.byref(desc), ctypes.byref(h)))
+    _LAYERS[h.value] = (d_model, n_neurons, n_q_heads, n_kv_groups, head_dim, dtype)
     return h.value
 
 
 def dtp_layer_destroy(layer):
     _check(lib().dtp_layer_destroy(layer))
+    _LAYERS.pop(layer, None)
+
+
+def _layer_shape(layer):
+    if layer not in _LAYERS:
+        raise ValueError("not a layer handle returned by dtp_layer_create (or already destroyed)")
+    return _LAYERS[layer]
 
 
 def dtp_layer_set_weights(layer, w_o, gamma, w_gate, w_up, w_down, stream=None):
-    _check(lib().dtp_layer_set_weights(layer, _ptr(w_o), _ptr(gamma), _ptr(w_gate), _ptr(w_up),
-                                       _ptr(w_down), _stream(stream)))
+    d, I, H, G, dh, dt = _layer_shape(layer)
+    ad = _act_dtypes(dt)
+    _check(lib().dtp_layer_set_weights(layer, _dev(w_o, "w_o", ad, d * H * dh), _dev(gamma, "gamma", ad, d),
+                                       _dev(w_gate, "w_gate", ad, I * d), _dev(w_up, "w_up", ad, I * d),
+                                       _dev(w_down, "w_down", ad, d * I), _stream(stream)))
+
+
+def _tokens(layer, x, attn, n_tokens, A):
+    d, I, H, G, dh, dt = _layer_shape(layer)
+    n = int(n_tokens)
+    ad = _act_dtypes(dt)
+    return (_dev(x, "x", ad, n * d), _dev(attn, "attn", ad, n * H * dh), n,
+            _dev(A, "A", ("float32",), G * I))
 
 
 def dtp_affinity_accumulate(layer, x, attn, n_tokens, A, stream=None):
-    _check(lib().dtp_affinity_accumulate(layer, _ptr(x), _ptr(attn), int(n_tokens), _ptr(A),
-                                         _stream(stream)))
+    _check(lib().dtp_affinity_accumulate(layer, *_tokens(layer, x, attn, n_tokens, A), _stream(stream)))
 
 
 def dtp_affinity_accumulate_add(layer, x, attn, n_tokens, A, stream=None):
-    _check(lib().dtp_affinity_accumulate_add(layer, _ptr(x), _ptr(attn), int(n_tokens), _ptr(A),
+    _check(lib().dtp_affinity_accumulate_add(layer, *_tokens(layer, x, attn, n_tokens, A),
                                              _stream(stream)))
 
 
 def dtp_affinity_accumulate_down(layer, x, attn, x_next, rms_eps_next, n_tokens, A, s_down,
                                  stream=None):
-    _check(lib().dtp_affinity_accumulate_down(layer, _ptr(x), _ptr(attn), _ptr(x_next),
-                                              float(rms_eps_next), int(n_tokens), _ptr(A),
-                                              _ptr(s_down), _stream(stream)))
+    d, I, H, G, dh, dt = _layer_shape(layer)
+    px, pa, n, pA = _tokens(layer, x, attn, n_tokens, A)
+    _check(lib().dtp_affinity_accumulate_down(layer, px, pa, _dev(x_next, "x_next", _act_dtypes(dt), n * d),
+                                              float(rms_eps_next), n, pA,
+                                              _dev(s_down, "s_down", ("float32",), I), _stream(stream)))
 
 
 def dtp_down_weights(d_model, n_neurons, n_q_heads, n_kv_groups, head_dim, dtype, w_q, w_k, w_v,
                      gamma_next, w_down, B, stream=None):
+    ad = _act_dtypes(dtype)
+    d, I, HD, GD = d_model, n_neurons, n_q_heads * head_dim, n_kv_groups * head_dim
     _check(lib().dtp_down_weights(d_model, n_neurons, n_q_heads, n_kv_groups, head_dim, int(dtype),
-                                  _ptr(w_q), _ptr(w_k), _ptr(w_v), _ptr(gamma_next), _ptr(w_down),
-                                  _ptr(B), _stream(stream)))
+                                  _dev(w_q, "w_q", ad, HD * d), _dev(w_k, "w_k", ad, GD * d),
+                                  _dev(w_v, "w_v", ad, GD * d), _dev(gamma_next, "gamma_next", ad, d),
+                                  _dev(w_down, "w_down", ad, d * I),
+                                  _dev(B, "B", ("float32",), n_kv_groups * I), _stream(stream)))
 
 
 def dtp_down_affinity(n_neurons, n_kv_groups, s_down, B, A_down, stream=None):
-    _check(lib().dtp_down_affinity(n_neurons, n_kv_groups, _ptr(s_down), _ptr(B), _ptr(A_down),
-                                   _stream(stream)))
+    n = n_neurons * n_kv_groups
+    f = ("float32",)
+    _check(lib().dtp_down_affinity(n_neurons, n_kv_groups, _dev(s_down, "s_down", f, n_neurons),
+                                   _dev(B, "B", f, n), _dev(A_down, "A_down", f, n), _stream(stream)))
 
 
 def dtp_layer_profile(layer, enable):
@@ -212,7 +280,9 @@ def dtp_encode_affinity(A):
 
 def dtp_encode_affinity_device(A, Q, stream=None):
     """A (fp32) and Q (int64, same number of elements) are device tensors; Q is written."""
-    _check(lib().dtp_encode_affinity_device(_ptr(A), A.numel(), _ptr(Q), _stream(stream)))
+    n = A.numel()
+    _check(lib().dtp_encode_affinity_device(_dev(A, "A", ("float32",), n), n,
+                                            _dev(Q, "Q", ("int64",), n), _stream(stream)))
     return Q
 
 
@@ -220,8 +290,12 @@ def dtp_partition_scores(G, I, L, Q_up, nu, Q_down_prev=None, nu_prev=None, mini
                          scores=None, stream=None):
     """Q_up, nu (and Q_down_prev, nu_prev) and scores are device tensors; returns best rank."""
     best = _I64()
-    _check(lib().dtp_partition_scores(G, I, L, _ptr(Q_up), _ptr(nu), _ptr(Q_down_prev),
-                                      _ptr(nu_prev), int(bool(minimise)), _ptr(scores),
+    P = max(dtp_partition_count(G, L), 0)
+    _check(lib().dtp_partition_scores(G, I, L, _dev(Q_up, "Q_up", ("int64",), G * I),
+                                      _dev(nu, "nu", ("int32",), I),
+                                      _dev(Q_down_prev, "Q_down_prev", ("int64",), I * G, True),
+                                      _dev(nu_prev, "nu_prev", ("int32",), I, True),
+                                      int(bool(minimise)), _dev(scores, "scores", ("int64",), P),
                                       ctypes.byref(best), _stream(stream)))
     return best.value
 
@@ -253,7 +327,7 @@ def dtp_coordinate_ascent(N, G, I, L, A_up, A_down=None, max_sweeps=64, freeze_h
                           freeze_neurons=False, minimise=False, layer_mask=None, stream=None,
                           dual_ascent_neurons=False):
     """A_up [N,G,I] (and A_down [N-1,I,G]) are device tensors; returns a dict of host results."""
-    mask = None if layer_mask is None else np.ascontiguousarray(layer_mask, dtype=np.uint8)
+    mask = None if layer_mask is None else _host(layer_mask, "layer_mask", np.uint8, N)
     opt = dtp_ca_options(max_sweeps, int(freeze_heads), int(freeze_neurons), int(minimise),
                          _ptr(mask), int(dual_ascent_neurons))
     h = np.zeros((N, G), dtype=np.int32)
@@ -261,7 +335,9 @@ def dtp_coordinate_ascent(N, G, I, L, A_up, A_down=None, max_sweeps=64, freeze_h
     jf = _I64()
     j = ctypes.c_double()
     sw = _I32()
-    _check(lib().dtp_coordinate_ascent(N, G, I, L, _ptr(A_up), _ptr(A_down), ctypes.byref(opt),
+    f = ("float32",)
+    _check(lib().dtp_coordinate_ascent(N, G, I, L, _dev(A_up, "A_up", f, N * G * I),
+                                       _dev(A_down, "A_down", f, (N - 1) * I * G, True), ctypes.byref(opt),
                                        _ptr(h), _ptr(nu), ctypes.byref(jf), ctypes.byref(j),
                                        ctypes.byref(sw), _stream(stream)))
     return {"h": h, "nu": nu, "J_fixed": jf.value, "J": j.value, "sweeps": sw.value}
@@ -314,10 +390,13 @@ def dtp_apply_layout(d_model, n_neurons, n_q_heads, n_kv_groups, head_dim, dtype
                      dst, stream=None):
     """Permute a layer's weights: ``src`` and ``dst`` map WEIGHT_ORDER names to tensors."""
     desc = dtp_layer_desc(d_model, n_neurons, n_q_heads, n_kv_groups, head_dim, 0.0, int(dtype))
-    h = np.ascontiguousarray(h, dtype=np.int32)
-    nu = np.ascontiguousarray(nu, dtype=np.int32)
-    srcp = (ctypes.c_void_p * 7)(*[_ptr(src[k]) for k in WEIGHT_ORDER])
-    dstp = (ctypes.c_void_p * 7)(*[_ptr(dst[k]) for k in WEIGHT_ORDER])
+    h = _host(h, "h", np.int32, n_kv_groups)
+    nu = _host(nu, "nu", np.int32, n_neurons)
+    d, I, HD, GD = d_model, n_neurons, n_q_heads * head_dim, n_kv_groups * head_dim
+    sizes = dict(w_q=HD * d, w_k=GD * d, w_v=GD * d, w_o=d * HD, w_gate=I * d, w_up=I * d, w_down=d * I)
+    ad = _act_dtypes(dtype)
+    srcp = (ctypes.c_void_p * 7)(*[_dev(src[k], "src " + k, ad, sizes[k]) for k in WEIGHT_ORDER])
+    dstp = (ctypes.c_void_p * 7)(*[_dev(dst[k], "dst " + k, ad, sizes[k]) for k in WEIGHT_ORDER])
     _check(lib().dtp_apply_layout(ctypes.byref(desc), L, _ptr(h), _ptr(nu),
                                   ctypes.cast(srcp, ctypes.c_void_p), ctypes.cast(dstp, ctypes.c_void_p),
                                   _stream(stream)))

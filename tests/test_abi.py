@@ -34,7 +34,9 @@ def _expect(status, fn, *a, **k):
 
 @pytest.mark.parametrize("bad", [
     dict(d_model=0), dict(n_neurons=-1), dict(n_q_heads=6, n_kv_groups=4),
-    dict(head_dim=24), dict(d_model=72), dict(rms_eps=-1.0), dict(rms_eps=float("nan")),
+    dict(head_dim=24), dict(rms_eps=-1.0), dict(rms_eps=float("nan")),
+    # d_model must be a multiple of 16 (rows are read in 16-element pieces)
+    dict(d_model=72), dict(d_model=24), dict(d_model=8), dict(d_model=1000),
 ])
 def test_layer_create_rejects_bad_shapes(bad):
     kw = dict(d_model=64, n_neurons=128, n_q_heads=8, n_kv_groups=4, head_dim=16, rms_eps=1e-6,
@@ -124,3 +126,53 @@ def test_partition_scores_and_ascent_arguments_checked_before_gpu():
     _expect(dtp.DTP_ERR_INVALID_ARG, dtp.dtp_coordinate_ascent, 1, 8, 16, 4, 1, A_down=1)
     _expect(dtp.DTP_ERR_INVALID_ARG, dtp.dtp_coordinate_ascent, 2, 8, 16, 4, 1, max_sweeps=0)
     _expect(dtp.DTP_ERR_UNSUPPORTED, dtp.dtp_coordinate_ascent, 2, 32, 32, 16, 1)
+
+
+# ----------------------------------------------------------------------------- binding checks
+# The wrappers check every device argument before the library sees it: a contiguous torch
+# tensor on the GPU, of the right dtype, with enough elements.  These checks run on the
+# host, so CPU tensors and numpy arrays exercise them here without a GPU.
+def test_device_argument_must_be_a_gpu_tensor():
+    import torch
+    with pytest.raises(TypeError, match="torch tensor"):
+        dtp.dtp_coordinate_ascent(1, 8, 16, 4, np.ones((8, 16), np.float32))
+    with pytest.raises(ValueError, match="on the GPU"):
+        dtp.dtp_coordinate_ascent(1, 8, 16, 4, torch.ones(8, 16))
+    with pytest.raises(ValueError, match="on the GPU"):
+        dtp.dtp_down_affinity(16, 8, torch.ones(16), torch.ones(8, 16), torch.ones(16, 8))
+    with pytest.raises(ValueError, match="on the GPU"):
+        dtp.dtp_encode_affinity_device(torch.ones(4), torch.zeros(4, dtype=torch.int64))
+
+
+def test_device_argument_dtype_and_size_checked():
+    import torch
+    t = torch.ones(10)
+    with pytest.raises(ValueError, match="on the GPU"):
+        dtp._dev(t, "A", ("float32",), 10)
+
+    class FakeCuda(torch.Tensor):   # a CPU tensor that claims to be on the GPU
+        @property
+        def is_cuda(self):
+            return True
+    f32 = torch.ones(10).as_subclass(FakeCuda)
+    assert dtp._dev(f32, "A", ("float32",), 10) == f32.data_ptr()
+    with pytest.raises(ValueError, match="has 10 elements"):
+        dtp._dev(f32, "A", ("float32",), 11)
+    with pytest.raises(TypeError, match="dtype"):
+        dtp._dev(f32, "A", ("bfloat16",), 10)
+    with pytest.raises(ValueError, match="contiguous"):
+        dtp._dev(torch.ones(4, 4).t().as_subclass(FakeCuda), "A", ("float32",), 16)
+    assert dtp._dev(None, "A_down", ("float32",), 0, optional=True) is None
+    with pytest.raises(ValueError, match="required"):
+        dtp._dev(None, "A", ("float32",), 1)
+    assert dtp._dev(12345, "A", ("float32",), 1) == 12345   # raw address: the library checks it
+
+
+def test_layer_mask_must_have_one_entry_per_layer():
+    with pytest.raises(ValueError, match="layer_mask has 3 elements, expected 4"):
+        dtp.dtp_coordinate_ascent(4, 8, 16, 4, 1, layer_mask=[1, 0, 1])
+
+
+def test_layer_wrappers_reject_unknown_handles():
+    with pytest.raises(ValueError, match="layer handle"):
+        dtp.dtp_affinity_accumulate(123456, 1, 1, 10, 1)

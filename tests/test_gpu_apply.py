@@ -1,4 +1,4 @@
-"""GPU: applying a layout to a layer's weights (Section 3, "Problem").
+"""GPU: applying a layout to a layer's weights (Section 3, "The layout as a free variable").
 
 The library's permuted weights must equal the oracle's bit for bit (pure data movement),
 and the permuted layer must compute the same function: the paper checks a maximum logit

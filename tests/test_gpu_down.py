@@ -155,8 +155,11 @@ def test_down_requires_next_residual():
         x = torch.zeros(4, wl.d_model, device="cuda")
         a = torch.zeros(4, wl.attn_width, device="cuda")
         A = torch.zeros(wl.n_kv_groups, wl.n_neurons, device="cuda")
-        with pytest.raises(dtp.DtpError):
+        with pytest.raises(ValueError, match="x_next is required"):   # the binding's check
             dtp.dtp_affinity_accumulate_down(layer, x, a, None, 1e-6, 4, A, A)
+        st = dtp.lib().dtp_affinity_accumulate_down(layer, x.data_ptr(), a.data_ptr(), None, 1e-6, 4,
+                                                    A.data_ptr(), A.data_ptr(), None)
+        assert st == dtp.DTP_ERR_INVALID_ARG                          # the library's own
     finally:
         dtp.dtp_layer_destroy(layer)
 

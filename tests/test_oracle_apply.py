@@ -1,4 +1,4 @@
-"""Pins of the layout-application oracle (Section 3, "Problem").
+"""Pins of the layout-application oracle (Section 3, "The layout as a free variable").
 
 * the permuted layer computes the same function (fp64 decoder layer with GQA attention,
   per-head q/k norms, rotary embedding and a SwiGLU FFN), as the paper states;
