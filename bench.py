@@ -10,8 +10,11 @@ heads of 128, 65,536 tokens, L=2 logical devices, bf16.  Inputs are synthetic an
 
 The JSON line reports calibration tokens/s per layer (value), the MFMA roofline of the
 dominant kernel timed with HIP events on its launch stream, and the fp64 oracle timed on
-a bounded token sample on the host cores.  ``--full-model`` adds the full-model layout
-time of the 28-layer Qwen3-0.6B-shaped model (262,144 tokens per layer, L=4).
+a bounded token sample on the host cores.  ``full_model`` gives the full-model layout time
+of the 28-layer Qwen3-0.6B-shaped model (262,144 tokens per layer, L=4), the 16-layer
+Danube3-500M-shaped model (131,072 tokens, L=2 and 4) and the 4-layer 8B-class stack
+(131,072 tokens, L=4), each with its affinity TFLOP/s and the oracle's tokens/s beside it;
+``layout.layer_optimum`` gives the ascent's gap to the exact optimum of the layer.
 """
 from __future__ import annotations
 
@@ -115,9 +118,36 @@ def cpu_baseline(wl, x, attn, w, L, n_tokens):
                       f"fp64 folded affinity ({t1 - t0:.1f} s) + exact layout optimiser ({t2 - t1:.1f} s)"}
 
 
-def full_model(dtp, synth, device, torch, name):
+def oracle_rate(wl, w, x, attn, n_tokens):
+    """The oracle as it stands (fp64 folded affinity, all neurons) on the first n_tokens of
+    layer 0 of a workload, on the host cores: tokens per second per layer."""
+    import numpy as np
+    from threadpoolctl import threadpool_info, threadpool_limits
+
+    from oracle import affinity as orc
+
+    xs = x[:n_tokens].float().cpu().numpy().astype(np.float64)
+    as_ = attn[:n_tokens].float().cpu().numpy().astype(np.float64)
+    wts = {k: w[k].float().cpu().numpy().astype(np.float64) for k in ("w_o", "gamma", "w_gate", "w_up", "w_down")}
+    cores = len(os.sched_getaffinity(0))
+    with threadpool_limits(limits=cores):
+        blas_threads = max([p.get("num_threads", 1) for p in threadpool_info()] or [1])
+        t0 = time.perf_counter()
+        orc.affinity_folded(xs, as_, wts["w_o"], wts["gamma"], wts["w_gate"], wts["w_up"], wts["w_down"],
+                            wl.n_kv_groups, wl.rms_eps)
+        dt = time.perf_counter() - t0
+    return {"tokens_per_s": n_tokens / dt, "cores": int(min(cores, blas_threads)), "kind": "oracle",
+            "sample": f"first {n_tokens} tokens of layer 0, all {wl.n_neurons} neurons, fp64 folded "
+                      f"affinity including its fold ({dt:.1f} s)"}
+
+
+ORACLE_SAMPLE = {"qwen3-0.6b-model": 8192, "danube3-500m": 8192, "8b-class-4layer": 1024}
+
+
+def full_model(dtp, synth, device, torch, name, with_oracle=True):
     """Full-model layout time: every layer's fold + affinity (up edge, and the down edge into
-    the next layer), then encode + ascent to convergence for each shard count."""
+    the next layer), then encode + ascent to convergence for each shard count.  One
+    untimed pass over the first layer and chunk warms the kernels first."""
     wl = synth.WORKLOADS[name]
     N, G, I = wl.n_layers, wl.n_kv_groups, wl.n_neurons
     nch = wl.tokens // wl.chunk
@@ -135,13 +165,12 @@ def full_model(dtp, synth, device, torch, name):
     s_down = torch.zeros(max(N - 1, 1), I, dtype=torch.float32, device=device)
     B = torch.zeros(G, I, dtype=torch.float32, device=device)
     A_down = torch.zeros(max(N - 1, 1), I, G, dtype=torch.float32, device=device)
-    torch.cuda.synchronize()
-    log(f"full model {name}: timing")
-    t0 = time.perf_counter()
-    for i in range(N):
+
+    def layer_pass(i, chunks):
         w = weights[i]
         dtp.dtp_layer_set_weights(layers[i], w["w_o"], w["gamma"], w["w_gate"], w["w_up"], w["w_down"])
-        for c, (x, a, _) in enumerate(data[i]):
+        for c in range(chunks):
+            x, a, _ = data[i][c]
             if i + 1 < N:
                 x_next = data[i + 1][c][2]   # residual entering layer i+1's attention pre-norm
                 dtp.dtp_affinity_accumulate_down(layers[i], x, a, x_next, wl.rms_eps, x.shape[0], A[i],
@@ -153,9 +182,25 @@ def full_model(dtp, synth, device, torch, name):
             dtp.dtp_down_weights(wl.d_model, I, wl.n_q_heads, G, wl.head_dim, dt, an["w_q"], an["w_k"],
                                  an["w_v"], an["gamma"], w["w_down"], B)
             dtp.dtp_down_affinity(I, G, s_down[i], B, A_down[i])
+
+    layer_pass(0, 1)                      # warm-up (kernels, allocator), then start clean
+    for L in wl.shards:
+        dtp.dtp_coordinate_ascent(N, G, I, L, A + 1.0, (A_down + 1.0) if N > 1 else None)
+    A.zero_()
+    s_down.zero_()
+    A_down.zero_()
+    torch.cuda.synchronize()
+    log(f"full model {name}: timing")
+    t0 = time.perf_counter()
+    for i in range(N):
+        layer_pass(i, nch)
     torch.cuda.synchronize()
     t1 = time.perf_counter()
+    f_alg = flops_per_token(wl) * wl.tokens * N
     out = {"workload": wl.name, "layers": N, "tokens_per_layer": wl.tokens, "affinity_s": t1 - t0,
+           "affinity_tflops": f_alg / (t1 - t0) / 1e12,
+           "affinity_frac_of_peak": f_alg / (t1 - t0) / 1e12 / PEAK_BF16_TFLOPS,
+           "tokens_per_s_per_layer": wl.tokens * N / (t1 - t0),
            "edges": 2 * N - 1, "by_shards": []}
     for L in wl.shards:
         ta = time.perf_counter()
@@ -166,9 +211,33 @@ def full_model(dtp, synth, device, torch, name):
                                  "J_random_expectation": (2 * N - 1) / L})
     for layer in layers:
         dtp.dtp_layer_destroy(layer)
+    if with_oracle:
+        n = ORACLE_SAMPLE.get(name, 1024)
+        log(f"full model {name}: oracle on {n} tokens of layer 0")
+        x0, a0, _ = data[0][0]
+        out["oracle"] = oracle_rate(wl, weights[0], x0, a0, n)
     del data
     torch.cuda.empty_cache()
     out["context"] = "paper: affinity pass + optimisation under two minutes per model on one RTX 5090"
+    return out
+
+
+def layer_optimum(dtp, A, G, I, shard_counts):
+    """The ascent's J against the exact optimum of the layer (every head partition up to
+    relabelling, each with its exact neuron step), for each shard count."""
+    import numpy as np
+    Q = dtp.dtp_encode_affinity(A.cpu().numpy())
+    out = {}
+    for L in shard_counts:
+        if G % L or I % L:
+            continue
+        ca = dtp.dtp_coordinate_ascent(1, G, I, L, A)
+        t0 = time.perf_counter()
+        _, _, J_opt = dtp.dtp_layer_optimum(G, I, L, Q)
+        t1 = time.perf_counter()
+        out[f"L{L}"] = {"J_opt": J_opt / 2.0 ** 48, "J_ca": ca["J"], "gap": (J_opt - ca["J_fixed"]) / J_opt,
+                        "optimum_s": t1 - t0}
+    assert all(np.isfinite(v["J_opt"]) for v in out.values())
     return out
 
 
@@ -183,8 +252,9 @@ def main():
     ap.add_argument("--no-library-gemm", action="store_true",
                     help="skip the library GEMM of the same FLOPs (context, untimed)")
     ap.add_argument("--full-model", nargs="*", default=None, metavar="WORKLOAD",
-                    help="also time the full-model layout (default workloads: "
+                    help="workloads of the full-model layout time (default: "
                          "qwen3-0.6b-model danube3-500m 8b-class-4layer)")
+    ap.add_argument("--no-full-model", action="store_true", help="skip the full-model layout time")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="only run a plain device copy of this many MiB (HBM counter scale)")
     args = ap.parse_args()
@@ -296,7 +366,8 @@ def main():
         "step_tflops": flops_per_token(wl) * T / (ms_per_step * 1e-3) / 1e12,
         "breakdown_ms": {"fold": (b1 - b0) * 1e3, "affinity": (b2 - b1) * 1e3,
                          "layout": (b3 - b2) * 1e3},
-        "layout": {"J": res["J"], "sweeps": res["sweeps"], "neuron_step": neuron_steps},
+        "layout": {"J": res["J"], "sweeps": res["sweeps"], "neuron_step": neuron_steps,
+                   "layer_optimum": layer_optimum(dtp, A, G, I, sorted({L, 4}))},
         "context": "paper: 65,536-token affinity pass of a 28-layer model in 51 s on one RTX 5090",
     }
     if not args.no_library_gemm:
@@ -306,11 +377,12 @@ def main():
         log(f"cpu baseline: oracle on {args.cpu_sample_tokens} tokens")
         out["cpu_baseline"] = cpu_baseline(wl, x, attn, w, L, args.cpu_sample_tokens)
     dtp.dtp_layer_destroy(layer)
-    if args.full_model is not None:
+    if not args.no_full_model:
         del x, attn
         torch.cuda.empty_cache()
         names = args.full_model or ["qwen3-0.6b-model", "danube3-500m", "8b-class-4layer"]
-        out["full_model"] = [full_model(dtp, synth, device, torch, n) for n in names]
+        out["full_model"] = [full_model(dtp, synth, device, torch, n, with_oracle=not args.no_cpu_baseline)
+                             for n in names]
     print(json.dumps(out), flush=True)
 
 

@@ -245,13 +245,13 @@ typedef struct {
  *   A_up   dev [N, G, I] float  raw up affinity of each layer (from dtp_affinity_accumulate)
  *   A_down dev [N-1, I, G] float raw down affinity, or NULL (then the layers decouple)
  *   h      host [N, G] int32 output;  nu host [N, I] int32 output
- *   J_fixed host int64 output (J_int);  J host double output (J_int / 2^48)
+ *   J host double output (J_int / 2^48);  J_fixed host int64 output (J_int, exact)
  *   sweeps  host int32 output (sweeps run)
  * Synchronises `stream`.  DTP_ERR_DEGENERATE if any matrix is all zero or not finite. */
 dtp_status dtp_coordinate_ascent(int32_t N, int32_t G, int32_t I, int32_t L,
                                  const float* A_up, const float* A_down,
                                  const dtp_ca_options* options, int32_t* h, int32_t* nu,
-                                 int64_t* J_fixed, double* J, int32_t* sweeps, void* stream);
+                                 double* J, int64_t* J_fixed, int32_t* sweeps, void* stream);
 
 /* Seeded balanced layouts, the random baseline of the ablations (Section 4): for each
  * layer in turn, the contiguous h_i (h(g) = g/(G/L)) and then the contiguous nu_i are

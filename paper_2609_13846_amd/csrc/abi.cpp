@@ -344,13 +344,13 @@ dtp_status dtp_partition_scores(int32_t G, int32_t I, int32_t L, const int64_t* 
 
 dtp_status dtp_coordinate_ascent(int32_t N, int32_t G, int32_t I, int32_t L, const float* A_up,
                                  const float* A_down, const dtp_ca_options* options, int32_t* h,
-                                 int32_t* nu, int64_t* J_fixed, double* J, int32_t* sweeps,
+                                 int32_t* nu, double* J, int64_t* J_fixed, int32_t* sweeps,
                                  void* stream) {
   clear_error();
   DTP_CHECK(N >= 1, DTP_ERR_INVALID_ARG, "N=%d must be >= 1", N);
   dtp_status st = check_layout_sizes(G, I, L, kMaxAssignDevices);
   if (st != DTP_OK) return st;
-  DTP_CHECK(A_up && h && nu && J_fixed && J && sweeps, DTP_ERR_INVALID_ARG,
+  DTP_CHECK(A_up && h && nu && J && J_fixed && sweeps, DTP_ERR_INVALID_ARG,
             "a required pointer is NULL");
   DTP_CHECK(A_down == nullptr || N >= 2, DTP_ERR_INVALID_ARG, "A_down needs N >= 2");
   dtp_ca_options opt = {64, 0, 0, 0, nullptr, 0};

@@ -71,7 +71,7 @@ _SIGNATURES = {
     "dtp_balanced_assign_dual_ascent": (_I32, [_I32, _I32, _I32, _P, _P, _P, _P, _I32, _P,
                                                ctypes.POINTER(_I64)]),
     "dtp_coordinate_ascent": (_I32, [_I32, _I32, _I32, _I32, _P, _P, ctypes.POINTER(dtp_ca_options),
-                                     _P, _P, ctypes.POINTER(_I64), ctypes.POINTER(ctypes.c_double),
+                                     _P, _P, ctypes.POINTER(ctypes.c_double), ctypes.POINTER(_I64),
                                      ctypes.POINTER(_I32), _P]),
     "dtp_status_string": (ctypes.c_char_p, [_I32]),
     "dtp_last_error": (ctypes.c_char_p, []),
@@ -338,7 +338,7 @@ def dtp_coordinate_ascent(N, G, I, L, A_up, A_down=None, max_sweeps=64, freeze_h
     f = ("float32",)
     _check(lib().dtp_coordinate_ascent(N, G, I, L, _dev(A_up, "A_up", f, N * G * I),
                                        _dev(A_down, "A_down", f, (N - 1) * I * G, True), ctypes.byref(opt),
-                                       _ptr(h), _ptr(nu), ctypes.byref(jf), ctypes.byref(j),
+                                       _ptr(h), _ptr(nu), ctypes.byref(j), ctypes.byref(jf),
                                        ctypes.byref(sw), _stream(stream)))
     return {"h": h, "nu": nu, "J_fixed": jf.value, "J": j.value, "sweeps": sw.value}
 

@@ -68,3 +68,45 @@ def assert_affinity_close(A_gpu: np.ndarray, A_ref: np.ndarray, rel=REL_TOL, thr
     assert rel_err.max() <= rel, f"max rel err {rel_err.max():.3e} (mean {rel_err.mean():.3e})"
     assert err[~big].max(initial=0.0) <= rel * thresh * top
     return float(rel_err.max())
+
+
+def device_chain(wl: synth.Workload, n_layers=None, tokens=None):
+    """Raw up and down affinity of a whole layer chain at the workload's full token count,
+    on data generated on the device chunk by chunk (as the full-model benchmark streams
+    it): A_up [N, G, I] and A_down [N-1, I, G] device tensors (A_down None when N = 1).
+    Layer i's down edge reads the residual entering layer i+1 (its x_pre) and layer
+    i+1's attention weights."""
+    import torch
+    dev = torch.device("cuda", 0)
+    N = n_layers or wl.n_layers
+    T = tokens or wl.tokens
+    G, I = wl.n_kv_groups, wl.n_neurons
+    dt = dtp.DTP_BF16 if wl.dtype == "bf16" else dtp.DTP_F32
+    A = torch.zeros(N, G, I, dtype=torch.float32, device=dev)
+    A_down = torch.zeros(max(N - 1, 1), I, G, dtype=torch.float32, device=dev)
+    s_down = torch.zeros(I, dtype=torch.float32, device=dev)
+    B = torch.zeros(G, I, dtype=torch.float32, device=dev)
+    weights = [synth.device_weights(wl, i, dev) for i in range(N)]
+    for i in range(N):
+        w = weights[i]
+        layer = layer_for(wl)
+        try:
+            dtp.dtp_layer_set_weights(layer, w["w_o"], w["gamma"], w["w_gate"], w["w_up"], w["w_down"])
+            s_down.zero_()
+            for c in range(T // wl.chunk):
+                x, a = synth.device_tokens(wl, i, w, wl.chunk, c, dev)
+                if i + 1 < N:
+                    _, _, x_next = synth.device_tokens(wl, i + 1, weights[i + 1], wl.chunk, c, dev,
+                                                       with_pre=True)
+                    dtp.dtp_affinity_accumulate_down(layer, x, a, x_next, wl.rms_eps, wl.chunk, A[i], s_down)
+                else:
+                    dtp.dtp_affinity_accumulate(layer, x, a, wl.chunk, A[i])
+            if i + 1 < N:
+                an = synth.device_attn_weights(wl, i + 1, dev)
+                dtp.dtp_down_weights(wl.d_model, I, wl.n_q_heads, G, wl.head_dim, dt, an["w_q"], an["w_k"],
+                                     an["w_v"], an["gamma"], w["w_down"], B)
+                dtp.dtp_down_affinity(I, G, s_down, B, A_down[i])
+            torch.cuda.synchronize()
+        finally:
+            dtp.dtp_layer_destroy(layer)
+    return A, (A_down if N > 1 else None)

@@ -3,16 +3,15 @@
 The token statistic s_down comes out of the affinity pass (dtp_affinity_accumulate_down),
 the weight factor B from dtp_down_weights, and S_down = s * B from dtp_down_affinity.
 
-Tolerance.  The paper fixes none for S_down; it is derived from the arithmetic.  The
-operating point contracts x with W' = gamma * W rounded to bf16 (2^-9 relative per
-element), so g and u carry a relative error of up to kappa * 2^-9, kappa being the
-cancellation ratio sum_j |W'_kj n_j| / |g|, and alpha^2 doubles it.  On few tokens a
-neuron's statistic can be dominated by one cancelling token: an fp64 emulation of exactly
-that rounding differs from the exact oracle by up to 1.1e-2 on the shapes below (129-600
-tokens).  So s_down and S_down are held to 2e-2 relative on entries above 1e-3 of the
-maximum, and in addition to 1e-4 against that emulation, which shows the remaining
-difference is the operand rounding and nothing else.  B (bf16 gamma' * w^d_k, fp32 sums)
-is held to the up affinity's 1e-2.
+Bar.  The target's 1e-2 relative error on entries above 1e-3 of the maximum, checked
+entry by entry under the rounding model of tests/error_model.py: the operating point
+contracts x with W' = gamma * W rounded to bf16 and B contracts the next layer's
+projection with gamma' * w^d rounded to bf16, so each entry has a first-order error of
+standard deviation sigma computed from the inputs alone.  Every entry must lie within its
+model bound (6 sigma plus the second-order terms); entries whose bound fits inside 1e-2
+are held to 1e-2; the others (a neuron whose statistic one cancelling token dominates)
+are exempted and counted.  B, whose entries are well conditioned, is also held to 1e-2
+on every entry.  The fp32 path has no such rounding and is held to 1e-2 throughout.
 """
 import numpy as np
 import pytest
@@ -20,9 +19,8 @@ import pytest
 from oracle import affinity as orc_up
 from oracle import down as orc
 from paper_2609_13846_amd import dtp, synth
+from tests import error_model as em
 from tests.helpers import assert_affinity_close, layer_for, oracle_inputs, torch_dev
-
-DOWN_REL_TOL = 2e-2
 
 pytestmark = pytest.mark.gpu
 
@@ -71,19 +69,6 @@ def _gpu(wl, w, x, a, x_next, an, chunks=None):
         dtp.dtp_layer_destroy(layer)
 
 
-def _stat_with_bf16_operands(wl, w, x, x_next):
-    """s_down with the operating point's W' = gamma * W rounded to bf16, in fp64."""
-    f = synth.to_f64
-    wg = f(synth.round_to_bf16_bits(f(w.w_gate) * f(w.gamma)[None, :]))
-    wu = f(synth.round_to_bf16_bits(f(w.w_up) * f(w.gamma)[None, :]))
-    X = f(x)
-    r = orc_up.rms(X, wl.rms_eps)
-    g = X @ wg.T / r[:, None]
-    u = X @ wu.T / r[:, None]
-    rn = orc_up.rms(f(x_next), wl.rms_eps)
-    return np.sum((orc_up.silu(g) * u / rn[:, None]) ** 2, axis=0)
-
-
 def _oracle(wl, w, x, x_next, an):
     f = synth.to_f64
     kw = dict(x=f(x), gamma=f(w.gamma), w_gate=f(w.w_gate), w_up=f(w.w_up), eps=wl.rms_eps,
@@ -111,12 +96,25 @@ def test_down_edge_matches_oracle(name, over, T, chunks):
     w, x, a, x_next, an = _inputs(wl, T)
     A, s, B, S, A_plain = _gpu(wl, w, x, a, x_next, an, chunks)
     s_ref, B_ref = _oracle(wl, w, x, x_next, an)
-    assert_affinity_close(s[None, :], s_ref[None, :], rel=DOWN_REL_TOL)
     assert_affinity_close(B, B_ref)
-    assert_affinity_close(S, s_ref[:, None] * B_ref.T, rel=DOWN_REL_TOL)
     if wl.dtype == "bf16":
-        s_emu = _stat_with_bf16_operands(wl, w, x, x_next)
-        assert_affinity_close(s[None, :], s_emu[None, :], rel=1e-4)
+        f = synth.to_f64
+        s_m, s_sig, s_sec = em.down_stat_error(f(x), f(w.gamma), f(w.w_gate), f(w.w_up), wl.rms_eps,
+                                               f(x_next), wl.rms_eps)
+        B_m, B_sig, B_sec = em.down_weight_error(f(an.w_q), f(an.w_k), f(an.w_v), f(an.gamma),
+                                                 f(w.w_down), wl.n_q_heads, wl.n_kv_groups)
+        np.testing.assert_allclose(s_m, s_ref, rtol=1e-10)
+        rs = em.check_entrywise(s[None, :], s_ref[None, :], s_sig[None, :], s_sec[None, :], label="s_down")
+        rb = em.check_entrywise(B, B_ref, B_sig, B_sec, label="B")
+        # S = s B: the two roundings are independent
+        S_ref = s_ref[:, None] * B_ref.T
+        S_sig = np.sqrt((B_ref.T * s_sig[:, None]) ** 2 + (s_ref[:, None] * B_sig.T) ** 2)
+        S_sec = B_ref.T * s_sec[:, None] + s_ref[:, None] * B_sec.T + s_sig[:, None] * B_sig.T
+        rS = em.check_entrywise(S, S_ref, S_sig, S_sec, label="S_down")
+        print(f"[gpu] down {name} T={T}: s_down {rs}; B {rb}; S_down {rS}", flush=True)
+    else:
+        assert_affinity_close(s[None, :], s_ref[None, :])
+        assert_affinity_close(S, s_ref[:, None] * B_ref.T)
     # the down statistic rides along without changing the up affinity
     np.testing.assert_array_equal(A, A_plain)
 
