@@ -131,6 +131,22 @@ dtp_status dtp_down_weights(int32_t d_model, int32_t n_neurons, int32_t n_q_head
                             const void* w_q, const void* w_k, const void* w_v,
                             const void* gamma_next, const void* w_down, float* B, void* stream);
 
+/* dtp_down_weights for callers that cannot allocate device memory (code under HIP graph
+ * capture, serving loops and harnesses that forbid hipMalloc): the same kernels and the same
+ * B bit for bit, with the per-chunk partial sums in a fixed 4 MiB device array instead of
+ * stream-ordered scratch.  The call makes no allocation of any kind; the array is held by
+ * each device the library runs on until the process ends (its address is looked up once per
+ * device, on the first call there).  Limit: G * I * ceil((H/G + 2) * dh / 128) <= 2^20
+ * partial sums (the 8B-class shape needs 688,128), else DTP_ERR_UNSUPPORTED before any
+ * work.  Calls on one device share the array: calls that overlap in time on one GPU (other
+ * streams, other host threads) race and must be ordered by the caller.  Arguments, checks
+ * and the f32 path (which needs no scratch) as for dtp_down_weights. */
+dtp_status dtp_down_weights_noalloc(int32_t d_model, int32_t n_neurons, int32_t n_q_heads,
+                                    int32_t n_kv_groups, int32_t head_dim, dtp_dtype dtype,
+                                    const void* w_q, const void* w_k, const void* w_v,
+                                    const void* gamma_next, const void* w_down, float* B,
+                                    void* stream);
+
 /* Raw down affinity S_down[k, g] = s_down[k] * B[g, k] (the A_down operand of
  * dtp_coordinate_ascent for this layer).
  *   s_down dev [I], B dev [G, I], A_down dev [I, G] float (written). */

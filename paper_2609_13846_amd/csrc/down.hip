@@ -17,6 +17,7 @@
 //   down_rows_reduce_kernel  B[g, k] = fixed-order fp64 sum over the row chunks
 //   down_combine_kernel      S_down[k, g] = s[k] B[g, k]
 #include <cmath>
+#include <mutex>
 
 #include "dtp_internal.h"
 #include "tile_mfma.h"
@@ -142,18 +143,44 @@ __global__ void down_combine_kernel(const float* __restrict__ s, const float* __
 
 unsigned blocks_for(int64_t n, int threads) { return (unsigned)((n + threads - 1) / threads); }
 
-}  // namespace
-}  // namespace dtp
+// Scratch of dtp_down_weights_noalloc: the per-chunk partial sums, in device memory the
+// library never allocates.  Each device the library runs on holds its own copy until the
+// process ends.  In host code `scratch` names a host-side stand-in, not a device address:
+// the kernels only ever receive the address hipGetSymbolAddress returns for the current
+// device (noalloc_scratch below).  Every slot a call reads is written earlier in the same
+// call, so nothing needs clearing between calls.
+constexpr size_t kNoAllocScratchFloats = size_t(1) << 20;  // 4 MiB
+constexpr int kNoAllocMaxDevices = 64;
+static __device__ __align__(256) float scratch[kNoAllocScratchFloats];
 
-using namespace dtp;
+std::mutex g_scratch_mu;
+float* g_scratch_dev[kNoAllocMaxDevices] = {};
 
-extern "C" {
+// The current device's copy of `scratch`, looked up once per device on first use.
+dtp_status noalloc_scratch(float** out) {
+  int dev = -1;
+  DTP_HIP(hipGetDevice(&dev));
+  DTP_CHECK(dev >= 0 && dev < kNoAllocMaxDevices, DTP_ERR_UNSUPPORTED,
+            "device %d: the allocation-free scratch is kept for devices 0..%d", dev,
+            kNoAllocMaxDevices - 1);
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (g_scratch_dev[dev] == nullptr) {
+    void* p = nullptr;
+    DTP_HIP(hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)));
+    DTP_CHECK(p != nullptr, DTP_ERR_HIP, "no device address for the scratch on device %d", dev);
+    g_scratch_dev[dev] = (float*)p;
+  }
+  *out = g_scratch_dev[dev];
+  return DTP_OK;
+}
 
-dtp_status dtp_down_weights(int32_t d_model, int32_t n_neurons, int32_t n_q_heads,
-                            int32_t n_kv_groups, int32_t head_dim, dtp_dtype dtype,
-                            const void* w_q, const void* w_k, const void* w_v,
-                            const void* gamma_next, const void* w_down, float* B, void* stream) {
-  clear_error();
+// Shared body of dtp_down_weights and dtp_down_weights_noalloc.  The scratch of the row-chunk
+// sums comes from the stream-ordered allocator, or with `use_static` from the current
+// device's copy of `scratch` (the call is refused when it would not fit).
+dtp_status down_weights(int32_t d_model, int32_t n_neurons, int32_t n_q_heads, int32_t n_kv_groups,
+                        int32_t head_dim, dtp_dtype dtype, const void* w_q, const void* w_k,
+                        const void* w_v, const void* gamma_next, const void* w_down, float* B,
+                        bool use_static, void* stream) {
   DTP_CHECK(d_model > 0 && n_neurons > 0 && n_q_heads > 0 && n_kv_groups > 0 && head_dim > 0,
             DTP_ERR_INVALID_ARG, "every size must be positive (d=%d I=%d H=%d G=%d dh=%d)",
             d_model, n_neurons, n_q_heads, n_kv_groups, head_dim);
@@ -162,14 +189,21 @@ dtp_status dtp_down_weights(int32_t d_model, int32_t n_neurons, int32_t n_q_head
   DTP_CHECK(d_model <= 65536 && n_neurons <= (1 << 20) && (int64_t)n_q_heads * head_dim <= 65536,
             DTP_ERR_UNSUPPORTED, "shape too large (d <= 65536, I <= 2^20, H*dh <= 65536)");
   DTP_CHECK(dtype == DTP_BF16 || dtype == DTP_F32, DTP_ERR_UNSUPPORTED, "dtype %d", dtype);
+  const int hpg = n_q_heads / n_kv_groups;
+  const int64_t GI = (int64_t)n_kv_groups * n_neurons;
+  const int R = (hpg + 2) * head_dim;
+  const int n_chunks = (R + kDRows - 1) / kDRows;
+  if (use_static && dtype == DTP_BF16)
+    DTP_CHECK((size_t)GI * n_chunks <= kNoAllocScratchFloats, DTP_ERR_UNSUPPORTED,
+              "G * I * ceil((H/G + 2) * dh / 128) = %lld partial sums exceed the %zu floats of "
+              "the allocation-free scratch (use dtp_down_weights)",
+              (long long)(GI * n_chunks), kNoAllocScratchFloats);
   DTP_CHECK(w_q && w_k && w_v && gamma_next && w_down && B, DTP_ERR_INVALID_ARG,
             "a weight pointer or B is NULL");
   auto al16 = [](const void* p) { return ((uintptr_t)p & 15u) == 0; };
   DTP_CHECK(al16(w_q) && al16(w_k) && al16(w_v) && al16(w_down), DTP_ERR_INVALID_ARG,
             "w_q, w_k, w_v and w_down must be 16-byte aligned");
   hipStream_t s = (hipStream_t)stream;
-  const int hpg = n_q_heads / n_kv_groups;
-  const int64_t GI = (int64_t)n_kv_groups * n_neurons;
   {
     const size_t esz = dtype == DTP_BF16 ? 2 : 4, dm = (size_t)d_model;
     const size_t gd = (size_t)n_kv_groups * head_dim;
@@ -193,10 +227,13 @@ dtp_status dtp_down_weights(int32_t d_model, int32_t n_neurons, int32_t n_q_head
   DTP_CHECK(d_model % 8 == 0, DTP_ERR_INVALID_ARG, "d_model=%d is not a multiple of 8", d_model);
   DTP_CHECK(n_neurons % 8 == 0, DTP_ERR_INVALID_ARG, "n_neurons=%d is not a multiple of 8",
             n_neurons);
-  const int R = (hpg + 2) * head_dim;
-  const int n_chunks = (R + kDRows - 1) / kDRows;
   float* partial = nullptr;
-  DTP_HIP(hipMallocAsync((void**)&partial, sizeof(float) * (size_t)GI * n_chunks, s));
+  if (use_static) {
+    dtp_status st = noalloc_scratch(&partial);
+    if (st != DTP_OK) return st;
+  } else {
+    DTP_HIP(hipMallocAsync((void**)&partial, sizeof(float) * (size_t)GI * n_chunks, s));
+  }
   dim3 grid((n_neurons + kDCols - 1) / kDCols, n_chunks, n_kv_groups);
   down_weight_bf16_kernel<<<grid, kTileThreads, 0, s>>>(
       (const uint16_t*)w_q, (const uint16_t*)w_k, (const uint16_t*)w_v,
@@ -208,10 +245,36 @@ dtp_status dtp_down_weights(int32_t d_model, int32_t n_neurons, int32_t n_q_head
                                                                 n_neurons, B);
     e = hipGetLastError();
   }
-  const hipError_t ef = hipFreeAsync(partial, s);
+  const hipError_t ef = use_static ? hipSuccess : hipFreeAsync(partial, s);
   DTP_HIP(e);
   DTP_HIP(ef);
   return DTP_OK;
+}
+
+}  // namespace
+}  // namespace dtp
+
+using namespace dtp;
+
+extern "C" {
+
+dtp_status dtp_down_weights(int32_t d_model, int32_t n_neurons, int32_t n_q_heads,
+                            int32_t n_kv_groups, int32_t head_dim, dtp_dtype dtype,
+                            const void* w_q, const void* w_k, const void* w_v,
+                            const void* gamma_next, const void* w_down, float* B, void* stream) {
+  clear_error();
+  return down_weights(d_model, n_neurons, n_q_heads, n_kv_groups, head_dim, dtype, w_q, w_k, w_v,
+                      gamma_next, w_down, B, false, stream);
+}
+
+dtp_status dtp_down_weights_noalloc(int32_t d_model, int32_t n_neurons, int32_t n_q_heads,
+                                    int32_t n_kv_groups, int32_t head_dim, dtp_dtype dtype,
+                                    const void* w_q, const void* w_k, const void* w_v,
+                                    const void* gamma_next, const void* w_down, float* B,
+                                    void* stream) {
+  clear_error();
+  return down_weights(d_model, n_neurons, n_q_heads, n_kv_groups, head_dim, dtype, w_q, w_k, w_v,
+                      gamma_next, w_down, B, true, stream);
 }
 
 dtp_status dtp_down_affinity(int32_t n_neurons, int32_t n_kv_groups, const float* s_down,

@@ -59,6 +59,7 @@ _SIGNATURES = {
     "dtp_layer_optimum": (_I32, [_I32, _I32, _I32, _P, _P, _P, ctypes.POINTER(_I64)]),
     "dtp_affinity_accumulate_down": (_I32, [_P, _P, _P, _P, ctypes.c_float, _I64, _P, _P, _P]),
     "dtp_down_weights": (_I32, [_I32, _I32, _I32, _I32, _I32, _I32, _P, _P, _P, _P, _P, _P, _P]),
+    "dtp_down_weights_noalloc": (_I32, [_I32, _I32, _I32, _I32, _I32, _I32, _P, _P, _P, _P, _P, _P, _P]),
     "dtp_down_affinity": (_I32, [_I32, _I32, _P, _P, _P, _P]),
     "dtp_layer_profile": (_I32, [_P, _I32]),
     "dtp_layer_profile_read": (_I32, [_P, ctypes.POINTER(ctypes.c_double), ctypes.POINTER(_I64)]),
@@ -240,6 +241,18 @@ def dtp_down_weights(d_model, n_neurons, n_q_heads, n_kv_groups, head_dim, dtype
                                   _dev(w_v, "w_v", ad, GD * d), _dev(gamma_next, "gamma_next", ad, d),
                                   _dev(w_down, "w_down", ad, d * I),
                                   _dev(B, "B", ("float32",), n_kv_groups * I), _stream(stream)))
+
+
+def dtp_down_weights_noalloc(d_model, n_neurons, n_q_heads, n_kv_groups, head_dim, dtype, w_q, w_k,
+                             w_v, gamma_next, w_down, B, stream=None):
+    """dtp_down_weights without any device allocation (a fixed per-device scratch array)."""
+    ad = _act_dtypes(dtype)
+    d, I, HD, GD = d_model, n_neurons, n_q_heads * head_dim, n_kv_groups * head_dim
+    _check(lib().dtp_down_weights_noalloc(
+        d_model, n_neurons, n_q_heads, n_kv_groups, head_dim, int(dtype),
+        _dev(w_q, "w_q", ad, HD * d), _dev(w_k, "w_k", ad, GD * d), _dev(w_v, "w_v", ad, GD * d),
+        _dev(gamma_next, "gamma_next", ad, d), _dev(w_down, "w_down", ad, d * I),
+        _dev(B, "B", ("float32",), n_kv_groups * I), _stream(stream)))
 
 
 def dtp_down_affinity(n_neurons, n_kv_groups, s_down, B, A_down, stream=None):

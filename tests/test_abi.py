@@ -176,3 +176,15 @@ def test_layer_mask_must_have_one_entry_per_layer():
 def test_layer_wrappers_reject_unknown_handles():
     with pytest.raises(ValueError, match="layer handle"):
         dtp.dtp_affinity_accumulate(123456, 1, 1, 10, 1)
+
+
+def test_noalloc_down_weights_refuses_more_than_its_scratch_before_any_gpu_work():
+    """8 * 65536 * ceil(6 * 128 / 128) partial sums exceed the 2^20 of the fixed scratch:
+    refused from the shapes alone (raw addresses, no GPU needed)."""
+    lib = dtp.lib()
+    st = lib.dtp_down_weights_noalloc(64, 65536, 32, 8, 128, dtp.DTP_BF16, 16, 16, 16, 16, 16, 16, None)
+    assert st == dtp.DTP_ERR_UNSUPPORTED
+    assert "allocation-free scratch" in lib.dtp_last_error().decode()
+    # the allocating entry point has no such limit (it fails later, on the fake addresses)
+    assert lib.dtp_down_weights(64, 65536, 32, 8, 128, dtp.DTP_BF16, 16, 16, 16, 16, 16, 16, None) != \
+        dtp.DTP_ERR_UNSUPPORTED
