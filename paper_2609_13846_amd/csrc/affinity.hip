@@ -553,7 +553,11 @@ typedef _Float16 half2_t __attribute__((ext_vector_type(2)));
 template <int RB, int NB>
 struct Coefs<RB, NB, true> {
   uint32_t v[RB][NB][16];  // c1 in the low half, c2 in the high half
+  // a and b are first rounded to fp32 (the asm hides the products that made them), then to
+  // fp16: otherwise the compiler may fuse some products with the conversion (one rounding)
+  // and not others (two), and a token's coefficients would depend on its row slot.
   __device__ __forceinline__ void set(int rb, int nb, int i, float a, float b) {
+    asm("" : "+v"(a), "+v"(b));
     half2_t c;
     c.x = (_Float16)a;
     c.y = (_Float16)b;

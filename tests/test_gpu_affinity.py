@@ -123,6 +123,23 @@ def test_deterministic_and_chunk_additive():
     np.testing.assert_allclose(A3, A1, rtol=1e-5)
 
 
+def test_token_order_and_row_slot_do_not_matter():
+    """A is a sum over tokens: permuting them, or shifting every token to another row of
+    its tile by prepending all-zero tokens (u = 0 gives both coefficients zero, so such a
+    token adds exactly nothing), changes only the fp32 summation order.  Catches per-row
+    differences in the arithmetic, e.g. a coefficient rounded once in some rows and twice
+    in others."""
+    wl, w, x, a = case("qwen3-0.6b-layer", 1000)
+    announce("affinity: token permutation and row-slot shifts, T=1000")
+    A = hp.gpu_affinity(wl, w, x, a)
+    perm = np.random.default_rng(7).permutation(x.shape[0])
+    np.testing.assert_allclose(hp.gpu_affinity(wl, w, x[perm], a[perm]), A, rtol=1e-5)
+    for k in (1, 13, 31, 100):
+        xs = np.concatenate([np.zeros_like(x[:k]), x])
+        as_ = np.concatenate([np.zeros_like(a[:k]), a])
+        np.testing.assert_allclose(hp.gpu_affinity(wl, w, xs, as_), A, rtol=1e-5)
+
+
 @pytest.mark.parametrize("c", [2.0, 0.5])
 def test_power_of_two_head_scale_is_exact(c):
     """Scaling the query heads of one KV group by 2^k scales its row by 4^k bit for bit
