@@ -48,8 +48,9 @@ def kernel_sha() -> str:
 
 def _passes(out: str, steps: int):
     bench = [sys.executable, os.path.join(ROOT, "bench.py")]
-    timed = bench + ["--steps", str(steps), "--warmup", "2", "--no-cpu-baseline", "--no-library-gemm"]
-    short = bench + ["--steps", "2", "--warmup", "1", "--no-cpu-baseline", "--no-library-gemm"]
+    quiet = ["--no-cpu-baseline", "--no-library-gemm", "--no-full-model"]
+    timed = bench + ["--steps", str(steps), "--warmup", "2", *quiet]
+    short = bench + ["--steps", "2", "--warmup", "1", *quiet]
     copy = bench + ["--copy-calibration", str(COPY_MIB)]
     return [
         ("trace", ["--kernel-trace", "--stats"], timed, 300),
