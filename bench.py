@@ -112,10 +112,19 @@ def cpu_baseline(wl, x, attn, w, L, n_tokens):
         t1 = time.perf_counter()
         lay.coordinate_ascent([lay.encode(A.astype(np.float32))], None, L)
         t2 = time.perf_counter()
+        # the literal form (every p_h materialised in model space) on a smaller sample
+        n_lit = max(1, min(n_tokens, n_tokens // 24))
+        orc.affinity_literal(xs[:n_lit], as_[:n_lit], wts["w_o"], wts["gamma"], wts["w_gate"],
+                             wts["w_up"], wts["w_down"], wl.n_kv_groups, wl.rms_eps)
+        t3 = time.perf_counter()
     return {"value": n_tokens / (t2 - t0), "unit": "tokens/s", "cores": int(min(cores, blas_threads)),
             "kind": "oracle",
             "sample": f"first {n_tokens} tokens of the {wl.name} workload, all {wl.n_neurons} neurons: "
-                      f"fp64 folded affinity ({t1 - t0:.1f} s) + exact layout optimiser ({t2 - t1:.1f} s)"}
+                      f"fp64 folded affinity ({t1 - t0:.1f} s) + exact layout optimiser ({t2 - t1:.1f} s)",
+            "affinity_tokens_per_s": {
+                "folded": n_tokens / (t1 - t0),
+                "literal": n_lit / (t3 - t2),
+                "literal_sample": f"first {n_lit} tokens ({t3 - t2:.1f} s)"}}
 
 
 def oracle_rate(wl, w, x, attn, n_tokens):
@@ -360,6 +369,7 @@ def main():
                      "traffic_gbs": (pmc["bytes_per_launch"] / (avg_ms * 1e-3) / 1e9
                                      if pmc.get("bytes_per_launch") else None),
                      "mfma_busy_pmc": pmc.get("mfma_busy"), "clock_ghz_pmc": pmc.get("clock_ghz"),
+                     "wave_cycles_pmc": pmc.get("wave_cycles"),
                      "avg_launch_ms": avg_ms, "launches": launches,
                      "tokens_per_launch": T / max(launches_per_step, 1),
                      "flops_per_launch": f_launch},

@@ -14,7 +14,10 @@ own time limit, writing CSV output (no database files):
   SQ_VALU_MFMA_BUSY_CYCLES sums the matrix-core cycles of every SIMD (16 per
   ``v_mfma_f32_16x16x32_bf16``, 32 per ``32x32x16``), GRBM_GUI_ACTIVE the GPU cycles of each
   of the 8 XCDs, so the MFMA busy fraction is MFMA_BUSY / (GRBM_GUI_ACTIVE / 8 * 1024 SIMDs)
-  and GRBM_GUI_ACTIVE / 8 over the launch's duration is the clock it ran at.
+  and GRBM_GUI_ACTIVE / 8 over the launch's duration is the clock it ran at;
+* ``stall``: ``--kernel-trace`` with the SQ counters of where a wave's cycles go: issuing
+  VALU (MFMAs included), LDS and scalar instructions, waiting at ``s_waitcnt`` (any
+  counter, and LDS alone), all over the wave cycles (SQ_WAVE_CYCLES, same units).
 
 ``summarize`` writes a markdown summary of the kernel trace and the traffic of the
 affinity kernel (bytes per launch, counter scales applied) to ``profiles/``, plus the
@@ -38,6 +41,9 @@ COPY_MIB = 1024
 MFMA_COUNTERS = ["SQ_VALU_MFMA_BUSY_CYCLES", "SQ_BUSY_CYCLES", "SQ_INSTS_MFMA", "SQ_INSTS_VALU",
                  "SQ_INSTS_LDS", "SQ_LDS_BANK_CONFLICT", "SQ_LDS_IDX_ACTIVE", "SQ_WAVE_CYCLES",
                  "GRBM_GUI_ACTIVE"]
+STALL_COUNTERS = ["SQ_WAVE_CYCLES", "SQ_ACTIVE_INST_VALU", "SQ_ACTIVE_INST_LDS", "SQ_ACTIVE_INST_SCA",
+                  "SQ_ACTIVE_INST_ANY", "SQ_WAIT_INST_ANY", "SQ_WAIT_INST_LDS", "SQ_WAIT_ANY",
+                  "GRBM_GUI_ACTIVE"]
 N_XCD = 8
 N_SIMD = 1024
 
@@ -59,6 +65,7 @@ def _passes(out: str, steps: int):
         ("copyf", ["--pmc", "FETCH_SIZE"], copy, 120),
         ("copyw", ["--pmc", "WRITE_SIZE"], copy, 120),
         ("mfma", ["--kernel-trace", "--pmc", *MFMA_COUNTERS], short, 180),
+        ("stall", ["--kernel-trace", "--pmc", *STALL_COUNTERS], short, 180),
     ]
 
 
@@ -172,10 +179,32 @@ def summarize(d: str, profiles: str, workload: str, bench_cmd: str) -> None:
                   f"{m['SQ_INSTS_VALU']:.4g}; LDS instructions {m['SQ_INSTS_LDS']:.4g}",
                   f"- LDS bank conflicts: {m['SQ_LDS_BANK_CONFLICT'] / max(m['SQ_LDS_IDX_ACTIVE'], 1):.1%} "
                   f"of the LDS active cycles"]
+    sdir = os.path.join(d, "stall")
+    stall = {}
+    if os.path.isdir(sdir):
+        m2, _ = _counters(sdir, "affinity_bf16_kernel")
+        wc = m2["SQ_WAVE_CYCLES"]
+        stall = {k: m2[c] / wc for k, c in (("valu_issue", "SQ_ACTIVE_INST_VALU"),
+                                             ("lds_issue", "SQ_ACTIVE_INST_LDS"),
+                                             ("scalar_issue", "SQ_ACTIVE_INST_SCA"),
+                                             ("any_issue", "SQ_ACTIVE_INST_ANY"),
+                                             ("waitcnt", "SQ_WAIT_INST_ANY"),
+                                             ("waitcnt_lds", "SQ_WAIT_INST_LDS"),
+                                             ("wait_any", "SQ_WAIT_ANY"))}
+        lines += ["", "## Where a wave's cycles go (--pmc, one pass)", "",
+                  f"Counters: {', '.join(STALL_COUNTERS)}; each as a share of SQ_WAVE_CYCLES "
+                  f"({wc:.4g} per launch).", "",
+                  f"- issuing VALU instructions (MFMAs included): {stall['valu_issue']:.1%}",
+                  f"- issuing LDS instructions: {stall['lds_issue']:.1%}; scalar: {stall['scalar_issue']:.1%}; "
+                  f"any: {stall['any_issue']:.1%}",
+                  f"- waiting at s_waitcnt: {stall['waitcnt']:.1%} (on LDS alone: {stall['waitcnt_lds']:.1%})",
+                  f"- waiting for anything (SQ_WAIT_ANY): {stall['wait_any']:.1%}"]
     open(os.path.join(profiles, name + ".md"), "w").write("\n".join(lines) + "\n")
     mf = {}
     if os.path.isdir(mdir):
         mf = {"mfma_busy": busy, "clock_ghz": clock, "mfma_insts_per_launch": m["SQ_INSTS_MFMA"]}
+    if stall:
+        mf["wave_cycles"] = stall
     rec = {"kernel": "affinity_bf16_kernel", "workload": workload, "kernel_sha": kernel_sha(),
            "fetch_bytes_per_launch": fetch_b, "write_bytes_per_launch": write_b,
            "bytes_per_launch": fetch_b + write_b, "fetch_scale": f_scale, "write_scale": w_scale,
