@@ -1,7 +1,7 @@
 """Collect and summarise rocprofv3 runs of bench.py (kernel timing and HBM traffic).
 
-    python -m paper_2609_13846_amd.rocprof collect --out gpurun_out/prof
-    python -m paper_2609_13846_amd.rocprof summarize --dir gpurun_out/prof --profiles profiles
+    python -m paper_2609_13846_amd.rocprof collect --out <dir>
+    python -m paper_2609_13846_amd.rocprof summarize --dir <dir> --profiles profiles
 
 ``collect`` runs six rocprofv3 passes of ``bench.py``, each in its own process with its
 own time limit, writing CSV output (no database files):
