@@ -30,6 +30,9 @@ def rand_A(rng, shape):
 @pytest.mark.parametrize("G,I,L,down,minimise", [
     (8, 3072, 4, False, False), (8, 3072, 4, True, False), (8, 3072, 2, True, False),
     (8, 4096, 2, False, True), (4, 128, 2, True, False), (8, 14336, 4, True, False),
+    # unusual group and device counts: 40,320, 12,870, 34,650, 2 and 1 partitions
+    (8, 512, 8, True, False), (16, 256, 2, False, False), (12, 96, 3, True, True),
+    (2, 8, 2, True, False), (4, 32, 1, True, False),
 ])
 def test_partition_scores_bit_exact(G, I, L, down, minimise):
     announce(f"partition scores G={G} I={I} L={L} down={down} min={minimise}")
@@ -49,6 +52,22 @@ def test_partition_scores_bit_exact(G, I, L, down, minimise):
     assert best == lay.best_partition(ref, minimise)
 
 
+def test_partition_scores_refuse_more_than_2_pow_24_partitions():
+    """G = 16 over L = 4 devices has 63,063,000 labelled partitions, beyond the 2^24 the
+    scoring supports: refused before any work, whatever the buffers."""
+    G, I, L = 16, 64, 4
+    assert dtp.dtp_partition_count(G, L) == 63063000
+    Qu = torch.zeros(G, I, dtype=torch.int64, device="cuda")
+    nu = torch.zeros(I, dtype=torch.int32, device="cuda")
+    scores = torch.zeros(1, dtype=torch.int64, device="cuda")
+    with pytest.raises(dtp.DtpError) as e:
+        lib = dtp.lib()
+        best = dtp._I64()
+        dtp._check(lib.dtp_partition_scores(G, I, L, Qu.data_ptr(), nu.data_ptr(), None, None, 0,
+                                            scores.data_ptr(), dtp.ctypes.byref(best), None))
+    assert e.value.status == dtp.DTP_ERR_UNSUPPORTED
+
+
 def test_partition_scores_ties_take_lowest_rank():
     announce("partition scores ties")
     G, I, L = 8, 64, 4
@@ -61,7 +80,8 @@ def test_partition_scores_ties_take_lowest_rank():
 
 
 @pytest.mark.parametrize("N,G,I,L,down", [(1, 8, 3072, 2, False), (4, 8, 3072, 4, True),
-                                          (3, 8, 4096, 2, True), (2, 4, 128, 2, True)])
+                                          (3, 8, 4096, 2, True), (2, 4, 128, 2, True),
+                                          (2, 8, 64, 8, True), (2, 16, 96, 2, True)])
 def test_coordinate_ascent_bit_exact(N, G, I, L, down):
     announce(f"coordinate ascent N={N} G={G} I={I} L={L} down={down}")
     rng = np.random.default_rng(N * 100 + L)
