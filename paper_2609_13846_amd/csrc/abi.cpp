@@ -104,20 +104,19 @@ dtp_status check_layout_sizes(int G, int I, int L, int max_devices) {
   return DTP_OK;
 }
 
-int64_t objective_int(int N, int G, int I, const std::vector<int64_t>& Qu,
-                      const std::vector<int64_t>& Qd, bool has_down,
-                      const std::vector<int32_t>& h, const std::vector<int32_t>& nu) {
+int64_t objective_int(int N, int G, int I, const int64_t* Qu, const int64_t* Qd, bool has_down,
+                      const int32_t* h, const int32_t* nu) {
   int64_t J = 0;
   for (int i = 0; i < N; ++i) {
-    const int64_t* q = Qu.data() + (size_t)i * G * I;
-    const int32_t* hi = h.data() + (size_t)i * G;
-    const int32_t* ni = nu.data() + (size_t)i * I;
+    const int64_t* q = Qu + (size_t)i * G * I;
+    const int32_t* hi = h + (size_t)i * G;
+    const int32_t* ni = nu + (size_t)i * I;
     for (int g = 0; g < G; ++g)
       for (int k = 0; k < I; ++k)
         if (hi[g] == ni[k]) J += q[(size_t)g * I + k];
     if (has_down && i + 1 < N) {
-      const int64_t* qd = Qd.data() + (size_t)i * I * G;
-      const int32_t* hn = h.data() + (size_t)(i + 1) * G;
+      const int64_t* qd = Qd + (size_t)i * I * G;
+      const int32_t* hn = h + (size_t)(i + 1) * G;
       for (int k = 0; k < I; ++k)
         for (int g = 0; g < G; ++g)
           if (ni[k] == hn[g]) J += qd[(size_t)k * G + g];
@@ -151,6 +150,66 @@ struct DevBuf {
   ~DevBuf() {
     if (p) (void)stream_free(p, s);
   }
+};
+
+// Pinned host blocks for the device <-> host copies of the coordinate ascent.  A copy
+// between device memory and pageable host memory goes through the runtime's staging
+// buffer and costs several times the kernels around it (the codes of one 8 x 3072 layer,
+// 196 KB, took longer than every kernel of the ascent together); from pinned memory it is
+// one transfer.  Blocks come from a process-wide free list and go back to it when the call
+// returns; they are never released, so the list holds at most one block per call that ran
+// concurrently (each as large as the largest such call needed).
+class PinnedPool {
+ public:
+  struct Block {
+    void* p = nullptr;
+    size_t bytes = 0;
+  };
+  Block take(size_t bytes) {
+    {
+      std::lock_guard<std::mutex> lock(mu_);
+      for (size_t i = 0; i < free_.size(); ++i)
+        if (free_[i].bytes >= bytes) {
+          const Block b = free_[i];
+          free_.erase(free_.begin() + (std::ptrdiff_t)i);
+          return b;
+        }
+    }
+    Block b;
+    b.bytes = std::max(bytes, (size_t)64 << 10);
+    if (hipHostMalloc(&b.p, b.bytes, hipHostMallocPortable) != hipSuccess) b = Block();
+    return b;
+  }
+  void give(const Block& b) {
+    if (b.p == nullptr) return;
+    std::lock_guard<std::mutex> lock(mu_);
+    free_.push_back(b);
+  }
+
+ private:
+  std::mutex mu_;
+  std::vector<Block> free_;
+};
+
+PinnedPool& pinned_pool() {
+  static PinnedPool* pool = new PinnedPool;  // lives until the process ends
+  return *pool;
+}
+
+// A pinned block for one call, or (if pinned memory cannot be had) pageable memory.
+struct HostStaging {
+  PinnedPool::Block pinned;
+  std::vector<char> pageable;
+  char* base = nullptr;
+  explicit HostStaging(size_t bytes) : pinned(pinned_pool().take(bytes)) {
+    if (pinned.p) {
+      base = (char*)pinned.p;
+    } else {
+      pageable.resize(bytes);
+      base = pageable.data();
+    }
+  }
+  ~HostStaging() { pinned_pool().give(pinned); }
 };
 
 }  // namespace
@@ -382,11 +441,17 @@ dtp_status dtp_coordinate_ascent(int32_t N, int32_t G, int32_t I, int32_t L, con
   st = launch_encode_unit_mass(A_up, N, A_down, has_down ? N - 1 : 0, (int64_t)G * I, qu_dev,
                                qd_dev, st_dev, s);
   if (st != DTP_OK) return st;
-  std::vector<EncodeStats> stats(nmat);
-  std::vector<int64_t> Qu(nup), Qd(ndown);
-  DTP_HIP(hipMemcpyAsync(stats.data(), st_dev, st_bytes, hipMemcpyDeviceToHost, s));
-  DTP_HIP(hipMemcpyAsync(Qu.data(), qu_dev, qu_bytes, hipMemcpyDeviceToHost, s));
-  if (has_down) DTP_HIP(hipMemcpyAsync(Qd.data(), qd_dev, qd_bytes, hipMemcpyDeviceToHost, s));
+  // Host mirror of [encode stats | Q_up | Q_down], then the staging of the uploaded nu and
+  // of the best ranks, in pinned memory: one copy brings the stats and codes back.
+  const size_t nu_bytes = sizeof(int32_t) * (size_t)N * I;
+  const size_t best_off = (st_bytes + qu_bytes + qd_bytes + nu_bytes + 7) / 8 * 8;
+  HostStaging host(best_off + sizeof(int64_t) * (size_t)N);
+  const EncodeStats* stats = (const EncodeStats*)host.base;
+  const int64_t* Qu = (const int64_t*)(host.base + st_bytes);
+  const int64_t* Qd = has_down ? Qu + nup : nullptr;
+  int32_t* nu_host = (int32_t*)(host.base + st_bytes + qu_bytes + qd_bytes);
+  const int64_t* best = (const int64_t*)(host.base + best_off);
+  DTP_HIP(hipMemcpyAsync(host.base, block.p, st_bytes + qu_bytes + qd_bytes, hipMemcpyDeviceToHost, s));
   DTP_HIP(hipStreamSynchronize(s));
   for (int m = 0; m < nmat; ++m) {
     st = m < N ? check_encode_stats(stats[m], "up affinity of layer", m)
@@ -414,7 +479,6 @@ dtp_status dtp_coordinate_ascent(int32_t N, int32_t G, int32_t I, int32_t L, con
   }
   auto moves = [&](int i) { return opt.layer_mask == nullptr || opt.layer_mask[i] != 0; };
   const bool minimise = opt.minimise != 0;
-  std::vector<int64_t> best(N);
   int64_t J_prev = 0;
   int sweep = 0;
   while (sweep < opt.max_sweeps) {
@@ -428,8 +492,8 @@ dtp_status dtp_coordinate_ascent(int32_t N, int32_t G, int32_t I, int32_t L, con
         for (int i = t; i < N; i += nthreads) {
           if (!moves(i)) continue;
           const bool dn = has_down && i + 1 < N;
-          neuron_gain(G, I, L, Qu.data() + (size_t)i * G * I, hs.data() + (size_t)i * G,
-                      dn ? Qd.data() + (size_t)i * I * G : nullptr,
+          neuron_gain(G, I, L, Qu + (size_t)i * G * I, hs.data() + (size_t)i * G,
+                      dn ? Qd + (size_t)i * I * G : nullptr,
                       dn ? hs.data() + (size_t)(i + 1) * G : nullptr, minimise, &M);
           if (opt.dual_ascent_neurons)
             balanced_assign_dual_ascent(I, L, M.data(), kDualAscentIterations, kDualAscentDecay,
@@ -447,11 +511,12 @@ dtp_status dtp_coordinate_ascent(int32_t N, int32_t G, int32_t I, int32_t L, con
       }
     }
     if (!opt.freeze_heads) {
-      DTP_HIP(hipMemcpyAsync(nu_dev, nus.data(), sizeof(int32_t) * (size_t)N * I,
-                             hipMemcpyHostToDevice, s));
+      // staged: the previous sweep's upload from nu_host ended at its synchronisation
+      std::memcpy(nu_host, nus.data(), nu_bytes);
+      DTP_HIP(hipMemcpyAsync(nu_dev, nu_host, nu_bytes, hipMemcpyHostToDevice, s));
       st = launch_partition_scores(ws, qu_dev, nu_dev, qd_dev, nu_dev, minimise ? 1 : 0, s);
       if (st != DTP_OK) return st;
-      DTP_HIP(hipMemcpyAsync(best.data(), ws.best, sizeof(int64_t) * N, hipMemcpyDeviceToHost, s));
+      DTP_HIP(hipMemcpyAsync((void*)best, ws.best, sizeof(int64_t) * N, hipMemcpyDeviceToHost, s));
       DTP_HIP(hipStreamSynchronize(s));
       for (int i = 0; i < N; ++i) {
         if (!moves(i)) continue;
@@ -460,12 +525,12 @@ dtp_status dtp_coordinate_ascent(int32_t N, int32_t G, int32_t I, int32_t L, con
         for (int g = 0; g < G; ++g) hs[(size_t)i * G + g] = table[(size_t)best[i] * G + g];
       }
     }
-    const int64_t Jc = objective_int(N, G, I, Qu, Qd, has_down, hs, nus);
+    const int64_t Jc = objective_int(N, G, I, Qu, Qd, has_down, hs.data(), nus.data());
     const bool improved = sweep == 1 || (minimise ? Jc < J_prev : Jc > J_prev);
     J_prev = Jc;
     if (!improved) break;
   }
-  // The uploads read host vectors that die on return.
+  // The uploads read host memory that is released on return.
   DTP_HIP(hipStreamSynchronize(s));
   std::memcpy(h, hs.data(), sizeof(int32_t) * hs.size());
   std::memcpy(nu, nus.data(), sizeof(int32_t) * nus.size());
@@ -514,11 +579,7 @@ dtp_status dtp_layout_objective(int32_t N, int32_t G, int32_t I, int32_t L, cons
     for (int l = 0; l < L; ++l)
       DTP_CHECK(cnt[l] == I / L, DTP_ERR_INVALID_ARG, "nu[%d] is not balanced", i);
   }
-  const size_t nup = (size_t)N * G * I, ndown = Q_down ? (size_t)(N - 1) * I * G : 0;
-  std::vector<int64_t> Qu(Q_up, Q_up + nup), Qd;
-  if (Q_down) Qd.assign(Q_down, Q_down + ndown);
-  std::vector<int32_t> hv(h, h + (size_t)N * G), nv(nu, nu + (size_t)N * I);
-  *J_fixed = objective_int(N, G, I, Qu, Qd, Q_down != nullptr, hv, nv);
+  *J_fixed = objective_int(N, G, I, Q_up, Q_down, Q_down != nullptr, h, nu);
   return DTP_OK;
 }
 
