@@ -40,7 +40,7 @@ typedef enum {
   DTP_ERR_INVALID_ARG = -1,  /* null pointer, bad size, shape constraint violated */
   DTP_ERR_UNSUPPORTED = -2,  /* a valid request outside what the library implements */
   DTP_ERR_DEGENERATE = -3,   /* affinity all zero, negative or non-finite */
-  DTP_ERR_NO_MEMORY = -4,    /* host or device allocation failed */
+  DTP_ERR_NO_MEMORY = -4,    /* host or device allocation failed, or a host thread could not start */
   DTP_ERR_HIP = -5           /* a HIP runtime call failed (message has the HIP string) */
 } dtp_status;
 

@@ -258,377 +258,397 @@ const char* dtp_last_error(void) { return g_last_error; }
 int64_t dtp_partition_count(int32_t G, int32_t L) { return count_partitions(G, L); }
 
 dtp_status dtp_partition_unrank(int32_t G, int32_t L, int64_t rank, int32_t* h) {
-  clear_error();
-  DTP_CHECK(h != nullptr, DTP_ERR_INVALID_ARG, "h is NULL");
-  const int64_t P = count_partitions(G, L);
-  DTP_CHECK(P > 0, DTP_ERR_INVALID_ARG, "no balanced partitions for G=%d, L=%d", G, L);
-  DTP_CHECK(rank >= 0 && rank < P, DTP_ERR_INVALID_ARG, "rank %lld outside [0, %lld)",
-            (long long)rank, (long long)P);
-  unrank_partition(G, L, rank, h);
-  return DTP_OK;
+  return guarded([&]() -> dtp_status {
+    clear_error();
+    DTP_CHECK(h != nullptr, DTP_ERR_INVALID_ARG, "h is NULL");
+    const int64_t P = count_partitions(G, L);
+    DTP_CHECK(P > 0, DTP_ERR_INVALID_ARG, "no balanced partitions for G=%d, L=%d", G, L);
+    DTP_CHECK(rank >= 0 && rank < P, DTP_ERR_INVALID_ARG, "rank %lld outside [0, %lld)",
+              (long long)rank, (long long)P);
+    unrank_partition(G, L, rank, h);
+    return DTP_OK;
+  });
 }
 
 dtp_status dtp_encode_affinity(const float* A, int64_t n, int64_t* Q) {
-  clear_error();
-  DTP_CHECK(A != nullptr && Q != nullptr, DTP_ERR_INVALID_ARG, "A or Q is NULL");
-  DTP_CHECK(n >= 1 && n <= (int64_t(1) << 20), DTP_ERR_INVALID_ARG,
-            "n=%lld outside [1, 2^20]", (long long)n);
-  return encode_unit_mass(A, n, Q);
+  return guarded([&]() -> dtp_status {
+    clear_error();
+    DTP_CHECK(A != nullptr && Q != nullptr, DTP_ERR_INVALID_ARG, "A or Q is NULL");
+    DTP_CHECK(n >= 1 && n <= (int64_t(1) << 20), DTP_ERR_INVALID_ARG,
+              "n=%lld outside [1, 2^20]", (long long)n);
+    return encode_unit_mass(A, n, Q);
+  });
 }
 
 dtp_status dtp_encode_affinity_device(const float* A, int64_t n, int64_t* Q, void* stream) {
-  clear_error();
-  DTP_CHECK(A != nullptr && Q != nullptr, DTP_ERR_INVALID_ARG, "A or Q is NULL");
-  DTP_CHECK(n >= 1 && n <= (int64_t(1) << 30), DTP_ERR_INVALID_ARG,
-            "n=%lld outside [1, 2^30]", (long long)n);
-  dtp_status st0;
-  if ((st0 = check_dev_buffer(A, sizeof(float) * (size_t)n, "A")) != DTP_OK ||
-      (st0 = check_dev_buffer(Q, sizeof(int64_t) * (size_t)n, "Q")) != DTP_OK)
-    return st0;
-  hipStream_t s = (hipStream_t)stream;
-  DevBuf stats_dev(s);
-  DTP_HIP(stream_alloc(&stats_dev.p, sizeof(EncodeStats), s));
-  dtp_status st = launch_encode_unit_mass(A, 1, nullptr, 0, n, Q, nullptr,
-                                          (EncodeStats*)stats_dev.p, s);
-  if (st != DTP_OK) return st;
-  EncodeStats stats;
-  DTP_HIP(hipMemcpyAsync(&stats, stats_dev.p, sizeof(EncodeStats), hipMemcpyDeviceToHost, s));
-  DTP_HIP(hipStreamSynchronize(s));
-  return check_encode_stats(stats, "matrix", 0);
+  return guarded([&]() -> dtp_status {
+    clear_error();
+    DTP_CHECK(A != nullptr && Q != nullptr, DTP_ERR_INVALID_ARG, "A or Q is NULL");
+    DTP_CHECK(n >= 1 && n <= (int64_t(1) << 30), DTP_ERR_INVALID_ARG,
+              "n=%lld outside [1, 2^30]", (long long)n);
+    dtp_status st0;
+    if ((st0 = check_dev_buffer(A, sizeof(float) * (size_t)n, "A")) != DTP_OK ||
+        (st0 = check_dev_buffer(Q, sizeof(int64_t) * (size_t)n, "Q")) != DTP_OK)
+      return st0;
+    hipStream_t s = (hipStream_t)stream;
+    DevBuf stats_dev(s);
+    DTP_HIP(stream_alloc(&stats_dev.p, sizeof(EncodeStats), s));
+    dtp_status st = launch_encode_unit_mass(A, 1, nullptr, 0, n, Q, nullptr,
+                                            (EncodeStats*)stats_dev.p, s);
+    if (st != DTP_OK) return st;
+    EncodeStats stats;
+    DTP_HIP(hipMemcpyAsync(&stats, stats_dev.p, sizeof(EncodeStats), hipMemcpyDeviceToHost, s));
+    DTP_HIP(hipStreamSynchronize(s));
+    return check_encode_stats(stats, "matrix", 0);
+  });
 }
 
 dtp_status dtp_balanced_assign(int32_t G, int32_t I, int32_t L, const int64_t* Q_up,
                                const int32_t* h, const int64_t* Q_down, const int32_t* h_next,
                                int32_t minimise, int32_t* nu, int64_t* value) {
-  clear_error();
-  dtp_status st = check_layout_sizes(G, I, L, kMaxAssignDevices);
-  if (st != DTP_OK) return st;
-  DTP_CHECK(Q_up && h && nu && value, DTP_ERR_INVALID_ARG, "a required pointer is NULL");
-  DTP_CHECK((Q_down == nullptr) == (h_next == nullptr), DTP_ERR_INVALID_ARG,
-            "Q_down and h_next must both be given or both be NULL");
-  if ((st = check_balanced(h, G, L, "h")) != DTP_OK) return st;
-  if (h_next && (st = check_balanced(h_next, G, L, "h_next")) != DTP_OK) return st;
-  std::vector<int64_t> M;
-  neuron_gain(G, I, L, Q_up, h, Q_down, h_next, minimise != 0, &M);
-  int64_t v = 0;
-  balanced_assign_exact(I, L, M.data(), nu, &v);
-  *value = minimise ? -v : v;
-  return DTP_OK;
+  return guarded([&]() -> dtp_status {
+    clear_error();
+    dtp_status st = check_layout_sizes(G, I, L, kMaxAssignDevices);
+    if (st != DTP_OK) return st;
+    DTP_CHECK(Q_up && h && nu && value, DTP_ERR_INVALID_ARG, "a required pointer is NULL");
+    DTP_CHECK((Q_down == nullptr) == (h_next == nullptr), DTP_ERR_INVALID_ARG,
+              "Q_down and h_next must both be given or both be NULL");
+    if ((st = check_balanced(h, G, L, "h")) != DTP_OK) return st;
+    if (h_next && (st = check_balanced(h_next, G, L, "h_next")) != DTP_OK) return st;
+    std::vector<int64_t> M;
+    neuron_gain(G, I, L, Q_up, h, Q_down, h_next, minimise != 0, &M);
+    int64_t v = 0;
+    balanced_assign_exact(I, L, M.data(), nu, &v);
+    *value = minimise ? -v : v;
+    return DTP_OK;
+  });
 }
 
 dtp_status dtp_balanced_assign_dual_ascent(int32_t G, int32_t I, int32_t L, const int64_t* Q_up,
                                            const int32_t* h, const int64_t* Q_down,
                                            const int32_t* h_next, int32_t minimise, int32_t* nu,
                                            int64_t* value) {
-  clear_error();
-  dtp_status st = check_layout_sizes(G, I, L, kMaxAssignDevices);
-  if (st != DTP_OK) return st;
-  DTP_CHECK(Q_up && h && nu && value, DTP_ERR_INVALID_ARG, "a required pointer is NULL");
-  DTP_CHECK((Q_down == nullptr) == (h_next == nullptr), DTP_ERR_INVALID_ARG,
-            "Q_down and h_next must both be given or both be NULL");
-  if ((st = check_balanced(h, G, L, "h")) != DTP_OK) return st;
-  if (h_next && (st = check_balanced(h_next, G, L, "h_next")) != DTP_OK) return st;
-  std::vector<int64_t> M;
-  neuron_gain(G, I, L, Q_up, h, Q_down, h_next, minimise != 0, &M);
-  int64_t v = 0;
-  balanced_assign_dual_ascent(I, L, M.data(), kDualAscentIterations, kDualAscentDecay, nu, &v);
-  *value = minimise ? -v : v;
-  return DTP_OK;
+  return guarded([&]() -> dtp_status {
+    clear_error();
+    dtp_status st = check_layout_sizes(G, I, L, kMaxAssignDevices);
+    if (st != DTP_OK) return st;
+    DTP_CHECK(Q_up && h && nu && value, DTP_ERR_INVALID_ARG, "a required pointer is NULL");
+    DTP_CHECK((Q_down == nullptr) == (h_next == nullptr), DTP_ERR_INVALID_ARG,
+              "Q_down and h_next must both be given or both be NULL");
+    if ((st = check_balanced(h, G, L, "h")) != DTP_OK) return st;
+    if (h_next && (st = check_balanced(h_next, G, L, "h_next")) != DTP_OK) return st;
+    std::vector<int64_t> M;
+    neuron_gain(G, I, L, Q_up, h, Q_down, h_next, minimise != 0, &M);
+    int64_t v = 0;
+    balanced_assign_dual_ascent(I, L, M.data(), kDualAscentIterations, kDualAscentDecay, nu, &v);
+    *value = minimise ? -v : v;
+    return DTP_OK;
+  });
 }
 
 dtp_status dtp_partition_scores(int32_t G, int32_t I, int32_t L, const int64_t* Q_up,
                                 const int32_t* nu, const int64_t* Q_down_prev,
                                 const int32_t* nu_prev, int32_t minimise, int64_t* scores,
                                 int64_t* best_rank, void* stream) {
-  clear_error();
-  dtp_status st = check_layout_sizes(G, I, L, 64);
-  if (st != DTP_OK) return st;
-  DTP_CHECK(Q_up && nu && scores && best_rank, DTP_ERR_INVALID_ARG, "a required pointer is NULL");
-  DTP_CHECK((Q_down_prev == nullptr) == (nu_prev == nullptr), DTP_ERR_INVALID_ARG,
-            "Q_down_prev and nu_prev must both be given or both be NULL");
-  const int64_t P = count_partitions(G, L);
-  DTP_CHECK(P > 0 && P <= kMaxPartitions, DTP_ERR_UNSUPPORTED,
-            "%lld partitions exceed the limit of %lld", (long long)P, (long long)kMaxPartitions);
-  if ((st = check_dev_buffer(Q_up, sizeof(int64_t) * (size_t)G * I, "Q_up")) != DTP_OK ||
-      (st = check_dev_buffer(nu, sizeof(int32_t) * (size_t)I, "nu")) != DTP_OK ||
-      (st = check_dev_buffer(Q_down_prev, sizeof(int64_t) * (size_t)I * G, "Q_down_prev", true)) != DTP_OK ||
-      (st = check_dev_buffer(nu_prev, sizeof(int32_t) * (size_t)I, "nu_prev", true)) != DTP_OK ||
-      (st = check_dev_buffer(scores, sizeof(int64_t) * (size_t)P, "scores")) != DTP_OK)
-    return st;
-  hipStream_t s = (hipStream_t)stream;
-  // A two-layer view: layer 0 is empty padding so that layer 1 reads Q_down_prev / nu_prev
-  // as its incoming down edge.  Without a down edge one layer suffices.
-  const bool down = Q_down_prev != nullptr;
-  ScoreWorkspace ws;
-  st = score_workspace_create(&ws, down ? 2 : 1, G, I, L, s);
-  if (st != DTP_OK) {
+  return guarded([&]() -> dtp_status {
+    clear_error();
+    dtp_status st = check_layout_sizes(G, I, L, 64);
+    if (st != DTP_OK) return st;
+    DTP_CHECK(Q_up && nu && scores && best_rank, DTP_ERR_INVALID_ARG, "a required pointer is NULL");
+    DTP_CHECK((Q_down_prev == nullptr) == (nu_prev == nullptr), DTP_ERR_INVALID_ARG,
+              "Q_down_prev and nu_prev must both be given or both be NULL");
+    const int64_t P = count_partitions(G, L);
+    DTP_CHECK(P > 0 && P <= kMaxPartitions, DTP_ERR_UNSUPPORTED,
+              "%lld partitions exceed the limit of %lld", (long long)P, (long long)kMaxPartitions);
+    if ((st = check_dev_buffer(Q_up, sizeof(int64_t) * (size_t)G * I, "Q_up")) != DTP_OK ||
+        (st = check_dev_buffer(nu, sizeof(int32_t) * (size_t)I, "nu")) != DTP_OK ||
+        (st = check_dev_buffer(Q_down_prev, sizeof(int64_t) * (size_t)I * G, "Q_down_prev", true)) != DTP_OK ||
+        (st = check_dev_buffer(nu_prev, sizeof(int32_t) * (size_t)I, "nu_prev", true)) != DTP_OK ||
+        (st = check_dev_buffer(scores, sizeof(int64_t) * (size_t)P, "scores")) != DTP_OK)
+      return st;
+    hipStream_t s = (hipStream_t)stream;
+    // A two-layer view: layer 0 is empty padding so that layer 1 reads Q_down_prev / nu_prev
+    // as its incoming down edge.  Without a down edge one layer suffices.
+    const bool down = Q_down_prev != nullptr;
+    ScoreWorkspace ws;
+    st = score_workspace_create(&ws, down ? 2 : 1, G, I, L, s);
+    if (st != DTP_OK) {
+      score_workspace_destroy(&ws);
+      return st;
+    }
+    DevBuf qbuf(s), nbuf(s);
+    const int64_t* qu = Q_up;
+    const int32_t* nl = nu;
+    if (down) {
+      // layer 0 gets zero codes; layer 1 is the real layer
+      const size_t qbytes = sizeof(int64_t) * (size_t)G * I;
+      const size_t nbytes = sizeof(int32_t) * (size_t)I;
+      hipError_t e = stream_alloc(&qbuf.p, 2 * qbytes, s);
+      if (e == hipSuccess) e = stream_alloc(&nbuf.p, 2 * nbytes, s);
+      if (e == hipSuccess) e = hipMemsetAsync(qbuf.p, 0, qbytes, s);
+      if (e == hipSuccess)
+        e = hipMemcpyAsync((char*)qbuf.p + qbytes, Q_up, qbytes, hipMemcpyDeviceToDevice, s);
+      if (e == hipSuccess) e = hipMemcpyAsync(nbuf.p, nu_prev, nbytes, hipMemcpyDeviceToDevice, s);
+      if (e == hipSuccess)
+        e = hipMemcpyAsync((char*)nbuf.p + nbytes, nu, nbytes, hipMemcpyDeviceToDevice, s);
+      if (e != hipSuccess) {
+        score_workspace_destroy(&ws);
+        return fail(DTP_ERR_HIP, "staging the two-layer view failed: %s", hipGetErrorString(e));
+      }
+      qu = (const int64_t*)qbuf.p;
+      nl = (const int32_t*)nbuf.p;
+    }
+    st = launch_partition_scores(ws, qu, nl, Q_down_prev, nl, minimise, s);
+    if (st == DTP_OK) {
+      const int layer = down ? 1 : 0;
+      hipError_t e = hipMemcpyAsync(scores, ws.scores + (size_t)layer * P, sizeof(int64_t) * P,
+                                    hipMemcpyDeviceToDevice, s);
+      if (e == hipSuccess)
+        e = hipMemcpyAsync(best_rank, ws.best + layer, sizeof(int64_t), hipMemcpyDeviceToHost, s);
+      if (e == hipSuccess) e = hipStreamSynchronize(s);
+      if (e != hipSuccess) st = fail(DTP_ERR_HIP, "partition scoring failed: %s", hipGetErrorString(e));
+    }
     score_workspace_destroy(&ws);
     return st;
-  }
-  DevBuf qbuf(s), nbuf(s);
-  const int64_t* qu = Q_up;
-  const int32_t* nl = nu;
-  if (down) {
-    // layer 0 gets zero codes; layer 1 is the real layer
-    const size_t qbytes = sizeof(int64_t) * (size_t)G * I;
-    const size_t nbytes = sizeof(int32_t) * (size_t)I;
-    hipError_t e = stream_alloc(&qbuf.p, 2 * qbytes, s);
-    if (e == hipSuccess) e = stream_alloc(&nbuf.p, 2 * nbytes, s);
-    if (e == hipSuccess) e = hipMemsetAsync(qbuf.p, 0, qbytes, s);
-    if (e == hipSuccess)
-      e = hipMemcpyAsync((char*)qbuf.p + qbytes, Q_up, qbytes, hipMemcpyDeviceToDevice, s);
-    if (e == hipSuccess) e = hipMemcpyAsync(nbuf.p, nu_prev, nbytes, hipMemcpyDeviceToDevice, s);
-    if (e == hipSuccess)
-      e = hipMemcpyAsync((char*)nbuf.p + nbytes, nu, nbytes, hipMemcpyDeviceToDevice, s);
-    if (e != hipSuccess) {
-      score_workspace_destroy(&ws);
-      return fail(DTP_ERR_HIP, "staging the two-layer view failed: %s", hipGetErrorString(e));
-    }
-    qu = (const int64_t*)qbuf.p;
-    nl = (const int32_t*)nbuf.p;
-  }
-  st = launch_partition_scores(ws, qu, nl, Q_down_prev, nl, minimise, s);
-  if (st == DTP_OK) {
-    const int layer = down ? 1 : 0;
-    hipError_t e = hipMemcpyAsync(scores, ws.scores + (size_t)layer * P, sizeof(int64_t) * P,
-                                  hipMemcpyDeviceToDevice, s);
-    if (e == hipSuccess)
-      e = hipMemcpyAsync(best_rank, ws.best + layer, sizeof(int64_t), hipMemcpyDeviceToHost, s);
-    if (e == hipSuccess) e = hipStreamSynchronize(s);
-    if (e != hipSuccess) st = fail(DTP_ERR_HIP, "partition scoring failed: %s", hipGetErrorString(e));
-  }
-  score_workspace_destroy(&ws);
-  return st;
+  });
 }
 
 dtp_status dtp_coordinate_ascent(int32_t N, int32_t G, int32_t I, int32_t L, const float* A_up,
                                  const float* A_down, const dtp_ca_options* options, int32_t* h,
                                  int32_t* nu, double* J, int64_t* J_fixed, int32_t* sweeps,
                                  void* stream) {
-  clear_error();
-  DTP_CHECK(N >= 1, DTP_ERR_INVALID_ARG, "N=%d must be >= 1", N);
-  dtp_status st = check_layout_sizes(G, I, L, kMaxAssignDevices);
-  if (st != DTP_OK) return st;
-  DTP_CHECK(A_up && h && nu && J && J_fixed && sweeps, DTP_ERR_INVALID_ARG,
-            "a required pointer is NULL");
-  DTP_CHECK(A_down == nullptr || N >= 2, DTP_ERR_INVALID_ARG, "A_down needs N >= 2");
-  dtp_ca_options opt = {64, 0, 0, 0, nullptr, 0};
-  if (options) opt = *options;
-  DTP_CHECK(opt.max_sweeps >= 1, DTP_ERR_INVALID_ARG, "max_sweeps=%d must be >= 1",
-            opt.max_sweeps);
-  const int64_t P = count_partitions(G, L);
-  DTP_CHECK(P > 0 && P <= kMaxPartitions, DTP_ERR_UNSUPPORTED, "too many partitions (%lld)",
-            (long long)P);
-  const bool has_down = A_down != nullptr;
-  const size_t nup = (size_t)N * G * I, ndown = has_down ? (size_t)(N - 1) * I * G : 0;
-  if ((st = check_dev_buffer(A_up, sizeof(float) * nup, "A_up")) != DTP_OK ||
-      (st = check_dev_buffer(A_down, sizeof(float) * ndown, "A_down", true)) != DTP_OK)
-    return st;
-  hipStream_t s = (hipStream_t)stream;
-
-  // Unit-mass codes of every matrix, computed on the device where the head step reads
-  // them; the host copy feeds the neuron step and J.  Layout of the scratch block:
-  // [encode stats | Q_up | Q_down | nu].
-  const int nmat = N + (has_down ? N - 1 : 0);
-  const size_t st_bytes = sizeof(EncodeStats) * nmat;
-  const size_t qu_bytes = sizeof(int64_t) * nup, qd_bytes = sizeof(int64_t) * ndown;
-  DevBuf block(s);
-  DTP_HIP(stream_alloc(&block.p, st_bytes + qu_bytes + qd_bytes + sizeof(int32_t) * (size_t)N * I, s));
-  EncodeStats* st_dev = (EncodeStats*)block.p;
-  int64_t* qu_dev = (int64_t*)((char*)block.p + st_bytes);
-  int64_t* qd_dev = has_down ? qu_dev + nup : nullptr;
-  int32_t* nu_dev = (int32_t*)((char*)qu_dev + qu_bytes + qd_bytes);
-  st = launch_encode_unit_mass(A_up, N, A_down, has_down ? N - 1 : 0, (int64_t)G * I, qu_dev,
-                               qd_dev, st_dev, s);
-  if (st != DTP_OK) return st;
-  // Host mirror of [encode stats | Q_up | Q_down], then the staging of the uploaded nu and
-  // of the best ranks, in pinned memory: one copy brings the stats and codes back.
-  const size_t nu_bytes = sizeof(int32_t) * (size_t)N * I;
-  const size_t best_off = (st_bytes + qu_bytes + qd_bytes + nu_bytes + 7) / 8 * 8;
-  HostStaging host(best_off + sizeof(int64_t) * (size_t)N);
-  const EncodeStats* stats = (const EncodeStats*)host.base;
-  const int64_t* Qu = (const int64_t*)(host.base + st_bytes);
-  const int64_t* Qd = has_down ? Qu + nup : nullptr;
-  int32_t* nu_host = (int32_t*)(host.base + st_bytes + qu_bytes + qd_bytes);
-  const int64_t* best = (const int64_t*)(host.base + best_off);
-  DTP_HIP(hipMemcpyAsync(host.base, block.p, st_bytes + qu_bytes + qd_bytes, hipMemcpyDeviceToHost, s));
-  DTP_HIP(hipStreamSynchronize(s));
-  for (int m = 0; m < nmat; ++m) {
-    st = m < N ? check_encode_stats(stats[m], "up affinity of layer", m)
-               : check_encode_stats(stats[m], "down affinity of layer", m - N);
+  return guarded([&]() -> dtp_status {
+    clear_error();
+    DTP_CHECK(N >= 1, DTP_ERR_INVALID_ARG, "N=%d must be >= 1", N);
+    dtp_status st = check_layout_sizes(G, I, L, kMaxAssignDevices);
     if (st != DTP_OK) return st;
-  }
+    DTP_CHECK(A_up && h && nu && J && J_fixed && sweeps, DTP_ERR_INVALID_ARG,
+              "a required pointer is NULL");
+    DTP_CHECK(A_down == nullptr || N >= 2, DTP_ERR_INVALID_ARG, "A_down needs N >= 2");
+    dtp_ca_options opt = {64, 0, 0, 0, nullptr, 0};
+    if (options) opt = *options;
+    DTP_CHECK(opt.max_sweeps >= 1, DTP_ERR_INVALID_ARG, "max_sweeps=%d must be >= 1",
+              opt.max_sweeps);
+    const int64_t P = count_partitions(G, L);
+    DTP_CHECK(P > 0 && P <= kMaxPartitions, DTP_ERR_UNSUPPORTED, "too many partitions (%lld)",
+              (long long)P);
+    const bool has_down = A_down != nullptr;
+    const size_t nup = (size_t)N * G * I, ndown = has_down ? (size_t)(N - 1) * I * G : 0;
+    if ((st = check_dev_buffer(A_up, sizeof(float) * nup, "A_up")) != DTP_OK ||
+        (st = check_dev_buffer(A_down, sizeof(float) * ndown, "A_down", true)) != DTP_OK)
+      return st;
+    hipStream_t s = (hipStream_t)stream;
 
-  ScoreWorkspace ws;
-  st = score_workspace_create(&ws, N, G, I, L, s);
-  if (st != DTP_OK) {
-    score_workspace_destroy(&ws);
-    return st;
-  }
-  struct WsGuard {
-    ScoreWorkspace* w;
-    ~WsGuard() { score_workspace_destroy(w); }
-  } guard{&ws};
-  const std::vector<uint8_t>& table = ws.host_table;
-
-  // Contiguous start.
-  std::vector<int32_t> hs((size_t)N * G), nus((size_t)N * I);
-  for (int i = 0; i < N; ++i) {
-    for (int g = 0; g < G; ++g) hs[(size_t)i * G + g] = g / (G / L);
-    for (int k = 0; k < I; ++k) nus[(size_t)i * I + k] = k / (I / L);
-  }
-  auto moves = [&](int i) { return opt.layer_mask == nullptr || opt.layer_mask[i] != 0; };
-  const bool minimise = opt.minimise != 0;
-  int64_t J_prev = 0;
-  int sweep = 0;
-  while (sweep < opt.max_sweeps) {
-    ++sweep;
-    if (!opt.freeze_neurons) {
-      // Neuron block: layers are independent given the heads; solve them in parallel.
-      const unsigned hw = std::max(1u, std::thread::hardware_concurrency());
-      const int nthreads = (int)std::min<unsigned>(hw, (unsigned)N);
-      auto work = [&](int t) {
-        std::vector<int64_t> M;
-        for (int i = t; i < N; i += nthreads) {
-          if (!moves(i)) continue;
-          const bool dn = has_down && i + 1 < N;
-          neuron_gain(G, I, L, Qu + (size_t)i * G * I, hs.data() + (size_t)i * G,
-                      dn ? Qd + (size_t)i * I * G : nullptr,
-                      dn ? hs.data() + (size_t)(i + 1) * G : nullptr, minimise, &M);
-          if (opt.dual_ascent_neurons)
-            balanced_assign_dual_ascent(I, L, M.data(), kDualAscentIterations, kDualAscentDecay,
-                                        nus.data() + (size_t)i * I, nullptr);
-          else
-            balanced_assign_exact(I, L, M.data(), nus.data() + (size_t)i * I, nullptr);
-        }
-      };
-      if (nthreads == 1) {
-        work(0);
-      } else {
-        std::vector<std::thread> pool;
-        for (int t = 0; t < nthreads; ++t) pool.emplace_back(work, t);
-        for (auto& th : pool) th.join();
-      }
-    }
-    if (!opt.freeze_heads) {
-      // staged: the previous sweep's upload from nu_host ended at its synchronisation
-      std::memcpy(nu_host, nus.data(), nu_bytes);
-      DTP_HIP(hipMemcpyAsync(nu_dev, nu_host, nu_bytes, hipMemcpyHostToDevice, s));
-      st = launch_partition_scores(ws, qu_dev, nu_dev, qd_dev, nu_dev, minimise ? 1 : 0, s);
+    // Unit-mass codes of every matrix, computed on the device where the head step reads
+    // them; the host copy feeds the neuron step and J.  Layout of the scratch block:
+    // [encode stats | Q_up | Q_down | nu].
+    const int nmat = N + (has_down ? N - 1 : 0);
+    const size_t st_bytes = sizeof(EncodeStats) * nmat;
+    const size_t qu_bytes = sizeof(int64_t) * nup, qd_bytes = sizeof(int64_t) * ndown;
+    DevBuf block(s);
+    DTP_HIP(stream_alloc(&block.p, st_bytes + qu_bytes + qd_bytes + sizeof(int32_t) * (size_t)N * I, s));
+    EncodeStats* st_dev = (EncodeStats*)block.p;
+    int64_t* qu_dev = (int64_t*)((char*)block.p + st_bytes);
+    int64_t* qd_dev = has_down ? qu_dev + nup : nullptr;
+    int32_t* nu_dev = (int32_t*)((char*)qu_dev + qu_bytes + qd_bytes);
+    st = launch_encode_unit_mass(A_up, N, A_down, has_down ? N - 1 : 0, (int64_t)G * I, qu_dev,
+                                 qd_dev, st_dev, s);
+    if (st != DTP_OK) return st;
+    // Host mirror of [encode stats | Q_up | Q_down], then the staging of the uploaded nu and
+    // of the best ranks, in pinned memory: one copy brings the stats and codes back.
+    const size_t nu_bytes = sizeof(int32_t) * (size_t)N * I;
+    const size_t best_off = (st_bytes + qu_bytes + qd_bytes + nu_bytes + 7) / 8 * 8;
+    HostStaging host(best_off + sizeof(int64_t) * (size_t)N);
+    const EncodeStats* stats = (const EncodeStats*)host.base;
+    const int64_t* Qu = (const int64_t*)(host.base + st_bytes);
+    const int64_t* Qd = has_down ? Qu + nup : nullptr;
+    int32_t* nu_host = (int32_t*)(host.base + st_bytes + qu_bytes + qd_bytes);
+    const int64_t* best = (const int64_t*)(host.base + best_off);
+    DTP_HIP(hipMemcpyAsync(host.base, block.p, st_bytes + qu_bytes + qd_bytes, hipMemcpyDeviceToHost, s));
+    DTP_HIP(hipStreamSynchronize(s));
+    for (int m = 0; m < nmat; ++m) {
+      st = m < N ? check_encode_stats(stats[m], "up affinity of layer", m)
+                 : check_encode_stats(stats[m], "down affinity of layer", m - N);
       if (st != DTP_OK) return st;
-      DTP_HIP(hipMemcpyAsync((void*)best, ws.best, sizeof(int64_t) * N, hipMemcpyDeviceToHost, s));
-      DTP_HIP(hipStreamSynchronize(s));
-      for (int i = 0; i < N; ++i) {
-        if (!moves(i)) continue;
-        DTP_CHECK(best[i] >= 0 && best[i] < P, DTP_ERR_HIP, "partition scoring returned rank %lld",
-                  (long long)best[i]);
-        for (int g = 0; g < G; ++g) hs[(size_t)i * G + g] = table[(size_t)best[i] * G + g];
-      }
     }
-    const int64_t Jc = objective_int(N, G, I, Qu, Qd, has_down, hs.data(), nus.data());
-    const bool improved = sweep == 1 || (minimise ? Jc < J_prev : Jc > J_prev);
-    J_prev = Jc;
-    if (!improved) break;
-  }
-  // The uploads read host memory that is released on return.
-  DTP_HIP(hipStreamSynchronize(s));
-  std::memcpy(h, hs.data(), sizeof(int32_t) * hs.size());
-  std::memcpy(nu, nus.data(), sizeof(int32_t) * nus.size());
-  *J_fixed = J_prev;
-  *J = (double)J_prev / (double)(int64_t(1) << kFracBits);
-  *sweeps = sweep;
-  return DTP_OK;
+
+    ScoreWorkspace ws;
+    st = score_workspace_create(&ws, N, G, I, L, s);
+    if (st != DTP_OK) {
+      score_workspace_destroy(&ws);
+      return st;
+    }
+    struct WsGuard {
+      ScoreWorkspace* w;
+      ~WsGuard() { score_workspace_destroy(w); }
+    } guard{&ws};
+    const std::vector<uint8_t>& table = ws.host_table;
+
+    // Contiguous start.
+    std::vector<int32_t> hs((size_t)N * G), nus((size_t)N * I);
+    for (int i = 0; i < N; ++i) {
+      for (int g = 0; g < G; ++g) hs[(size_t)i * G + g] = g / (G / L);
+      for (int k = 0; k < I; ++k) nus[(size_t)i * I + k] = k / (I / L);
+    }
+    auto moves = [&](int i) { return opt.layer_mask == nullptr || opt.layer_mask[i] != 0; };
+    const bool minimise = opt.minimise != 0;
+    int64_t J_prev = 0;
+    int sweep = 0;
+    while (sweep < opt.max_sweeps) {
+      ++sweep;
+      if (!opt.freeze_neurons) {
+        // Neuron block: layers are independent given the heads; solve them in parallel.
+        const unsigned hw = std::max(1u, std::thread::hardware_concurrency());
+        const int nthreads = (int)std::min<unsigned>(hw, (unsigned)N);
+        auto work = [&](int t) {
+          std::vector<int64_t> M;
+          for (int i = t; i < N; i += nthreads) {
+            if (!moves(i)) continue;
+            const bool dn = has_down && i + 1 < N;
+            neuron_gain(G, I, L, Qu + (size_t)i * G * I, hs.data() + (size_t)i * G,
+                        dn ? Qd + (size_t)i * I * G : nullptr,
+                        dn ? hs.data() + (size_t)(i + 1) * G : nullptr, minimise, &M);
+            if (opt.dual_ascent_neurons)
+              balanced_assign_dual_ascent(I, L, M.data(), kDualAscentIterations, kDualAscentDecay,
+                                          nus.data() + (size_t)i * I, nullptr);
+            else
+              balanced_assign_exact(I, L, M.data(), nus.data() + (size_t)i * I, nullptr);
+          }
+        };
+        if (nthreads == 1) {
+          work(0);
+        } else {
+          std::vector<std::thread> pool;
+          for (int t = 0; t < nthreads; ++t) pool.emplace_back(work, t);
+          for (auto& th : pool) th.join();
+        }
+      }
+      if (!opt.freeze_heads) {
+        // staged: the previous sweep's upload from nu_host ended at its synchronisation
+        std::memcpy(nu_host, nus.data(), nu_bytes);
+        DTP_HIP(hipMemcpyAsync(nu_dev, nu_host, nu_bytes, hipMemcpyHostToDevice, s));
+        st = launch_partition_scores(ws, qu_dev, nu_dev, qd_dev, nu_dev, minimise ? 1 : 0, s);
+        if (st != DTP_OK) return st;
+        DTP_HIP(hipMemcpyAsync((void*)best, ws.best, sizeof(int64_t) * N, hipMemcpyDeviceToHost, s));
+        DTP_HIP(hipStreamSynchronize(s));
+        for (int i = 0; i < N; ++i) {
+          if (!moves(i)) continue;
+          DTP_CHECK(best[i] >= 0 && best[i] < P, DTP_ERR_HIP, "partition scoring returned rank %lld",
+                    (long long)best[i]);
+          for (int g = 0; g < G; ++g) hs[(size_t)i * G + g] = table[(size_t)best[i] * G + g];
+        }
+      }
+      const int64_t Jc = objective_int(N, G, I, Qu, Qd, has_down, hs.data(), nus.data());
+      const bool improved = sweep == 1 || (minimise ? Jc < J_prev : Jc > J_prev);
+      J_prev = Jc;
+      if (!improved) break;
+    }
+    // The uploads read host memory that is released on return.
+    DTP_HIP(hipStreamSynchronize(s));
+    std::memcpy(h, hs.data(), sizeof(int32_t) * hs.size());
+    std::memcpy(nu, nus.data(), sizeof(int32_t) * nus.size());
+    *J_fixed = J_prev;
+    *J = (double)J_prev / (double)(int64_t(1) << kFracBits);
+    *sweeps = sweep;
+    return DTP_OK;
+  });
 }
 
 dtp_status dtp_random_layout(int32_t N, int32_t G, int32_t I, int32_t L, uint64_t seed,
                              int32_t* h, int32_t* nu) {
-  clear_error();
-  DTP_CHECK(N >= 1, DTP_ERR_INVALID_ARG, "N=%d must be >= 1", N);
-  dtp_status st = check_layout_sizes(G, I, L, kMaxGroups);
-  if (st != DTP_OK) return st;
-  DTP_CHECK(h && nu, DTP_ERR_INVALID_ARG, "h or nu is NULL");
-  uint64_t counter = 0;
-  for (int i = 0; i < N; ++i) {
-    int32_t* hi = h + (size_t)i * G;
-    int32_t* ni = nu + (size_t)i * I;
-    for (int g = 0; g < G; ++g) hi[g] = g / (G / L);
-    shuffle(hi, G, seed, &counter);
-    for (int k = 0; k < I; ++k) ni[k] = k / (I / L);
-    shuffle(ni, I, seed, &counter);
-  }
-  return DTP_OK;
+  return guarded([&]() -> dtp_status {
+    clear_error();
+    DTP_CHECK(N >= 1, DTP_ERR_INVALID_ARG, "N=%d must be >= 1", N);
+    dtp_status st = check_layout_sizes(G, I, L, kMaxGroups);
+    if (st != DTP_OK) return st;
+    DTP_CHECK(h && nu, DTP_ERR_INVALID_ARG, "h or nu is NULL");
+    uint64_t counter = 0;
+    for (int i = 0; i < N; ++i) {
+      int32_t* hi = h + (size_t)i * G;
+      int32_t* ni = nu + (size_t)i * I;
+      for (int g = 0; g < G; ++g) hi[g] = g / (G / L);
+      shuffle(hi, G, seed, &counter);
+      for (int k = 0; k < I; ++k) ni[k] = k / (I / L);
+      shuffle(ni, I, seed, &counter);
+    }
+    return DTP_OK;
+  });
 }
 
 dtp_status dtp_layout_objective(int32_t N, int32_t G, int32_t I, int32_t L, const int64_t* Q_up,
                                 const int64_t* Q_down, const int32_t* h, const int32_t* nu,
                                 int64_t* J_fixed) {
-  clear_error();
-  DTP_CHECK(N >= 1, DTP_ERR_INVALID_ARG, "N=%d must be >= 1", N);
-  dtp_status st = check_layout_sizes(G, I, L, kMaxGroups);
-  if (st != DTP_OK) return st;
-  DTP_CHECK(Q_up && h && nu && J_fixed, DTP_ERR_INVALID_ARG, "a required pointer is NULL");
-  DTP_CHECK(Q_down == nullptr || N >= 2, DTP_ERR_INVALID_ARG, "Q_down needs N >= 2");
-  for (int i = 0; i < N; ++i) {
-    if ((st = check_balanced(h + (size_t)i * G, G, L, "h")) != DTP_OK) return st;
-    std::vector<int32_t> cnt(L, 0);
-    for (int k = 0; k < I; ++k) {
-      const int32_t l = nu[(size_t)i * I + k];
-      DTP_CHECK(l >= 0 && l < L, DTP_ERR_INVALID_ARG, "nu[%d][%d] = %d is not a device", i, k, l);
-      ++cnt[l];
+  return guarded([&]() -> dtp_status {
+    clear_error();
+    DTP_CHECK(N >= 1, DTP_ERR_INVALID_ARG, "N=%d must be >= 1", N);
+    dtp_status st = check_layout_sizes(G, I, L, kMaxGroups);
+    if (st != DTP_OK) return st;
+    DTP_CHECK(Q_up && h && nu && J_fixed, DTP_ERR_INVALID_ARG, "a required pointer is NULL");
+    DTP_CHECK(Q_down == nullptr || N >= 2, DTP_ERR_INVALID_ARG, "Q_down needs N >= 2");
+    for (int i = 0; i < N; ++i) {
+      if ((st = check_balanced(h + (size_t)i * G, G, L, "h")) != DTP_OK) return st;
+      std::vector<int32_t> cnt(L, 0);
+      for (int k = 0; k < I; ++k) {
+        const int32_t l = nu[(size_t)i * I + k];
+        DTP_CHECK(l >= 0 && l < L, DTP_ERR_INVALID_ARG, "nu[%d][%d] = %d is not a device", i, k, l);
+        ++cnt[l];
+      }
+      for (int l = 0; l < L; ++l)
+        DTP_CHECK(cnt[l] == I / L, DTP_ERR_INVALID_ARG, "nu[%d] is not balanced", i);
     }
-    for (int l = 0; l < L; ++l)
-      DTP_CHECK(cnt[l] == I / L, DTP_ERR_INVALID_ARG, "nu[%d] is not balanced", i);
-  }
-  *J_fixed = objective_int(N, G, I, Q_up, Q_down, Q_down != nullptr, h, nu);
-  return DTP_OK;
+    *J_fixed = objective_int(N, G, I, Q_up, Q_down, Q_down != nullptr, h, nu);
+    return DTP_OK;
+  });
 }
 
 dtp_status dtp_layer_optimum(int32_t G, int32_t I, int32_t L, const int64_t* Q_up, int32_t* h,
                              int32_t* nu, int64_t* J_fixed) {
-  clear_error();
-  dtp_status st = check_layout_sizes(G, I, L, kMaxAssignDevices);
-  if (st != DTP_OK) return st;
-  DTP_CHECK(Q_up && h && nu && J_fixed, DTP_ERR_INVALID_ARG, "a required pointer is NULL");
-  const int64_t P = count_partitions(G, L);
-  DTP_CHECK(P > 0 && P <= kMaxPartitions, DTP_ERR_UNSUPPORTED, "too many partitions (%lld)",
-            (long long)P);
-  // One representative per partition up to device relabelling: labels first appear in
-  // the order 0, 1, ..., L-1.
-  const std::vector<uint8_t> table = enumerate_partitions(G, L);
-  std::vector<int64_t> reps;
-  for (int64_t r = 0; r < P; ++r) {
-    const uint8_t* hp = table.data() + (size_t)r * G;
-    int next = 0;
-    bool ok = true;
-    for (int g = 0; g < G && ok; ++g) {
-      if (hp[g] > next) ok = false;
-      else if (hp[g] == next) ++next;
+  return guarded([&]() -> dtp_status {
+    clear_error();
+    dtp_status st = check_layout_sizes(G, I, L, kMaxAssignDevices);
+    if (st != DTP_OK) return st;
+    DTP_CHECK(Q_up && h && nu && J_fixed, DTP_ERR_INVALID_ARG, "a required pointer is NULL");
+    const int64_t P = count_partitions(G, L);
+    DTP_CHECK(P > 0 && P <= kMaxPartitions, DTP_ERR_UNSUPPORTED, "too many partitions (%lld)",
+              (long long)P);
+    // One representative per partition up to device relabelling: labels first appear in
+    // the order 0, 1, ..., L-1.
+    const std::vector<uint8_t> table = enumerate_partitions(G, L);
+    std::vector<int64_t> reps;
+    for (int64_t r = 0; r < P; ++r) {
+      const uint8_t* hp = table.data() + (size_t)r * G;
+      int next = 0;
+      bool ok = true;
+      for (int g = 0; g < G && ok; ++g) {
+        if (hp[g] > next) ok = false;
+        else if (hp[g] == next) ++next;
+      }
+      if (ok) reps.push_back(r);
     }
-    if (ok) reps.push_back(r);
-  }
-  std::vector<int64_t> value(reps.size());
-  std::vector<std::vector<int32_t>> nus(reps.size(), std::vector<int32_t>(I));
-  auto solve = [&](size_t j) {
-    int32_t hh[kMaxGroups];
-    for (int g = 0; g < G; ++g) hh[g] = table[(size_t)reps[j] * G + g];
-    std::vector<int64_t> M;
-    neuron_gain(G, I, L, Q_up, hh, nullptr, nullptr, false, &M);
-    balanced_assign_exact(I, L, M.data(), nus[j].data(), &value[j]);
-  };
-  const unsigned hw = std::max(1u, std::min(16u, std::thread::hardware_concurrency()));
-  std::vector<std::thread> pool;
-  for (unsigned t = 0; t < hw; ++t)
-    pool.emplace_back([&, t] {
-      for (size_t j = t; j < reps.size(); j += hw) solve(j);
-    });
-  for (auto& th : pool) th.join();
-  size_t best = 0;  // first partition (lexicographic) attaining the maximum
-  for (size_t j = 1; j < reps.size(); ++j)
-    if (value[j] > value[best]) best = j;
-  for (int g = 0; g < G; ++g) h[g] = table[(size_t)reps[best] * G + g];
-  std::copy(nus[best].begin(), nus[best].end(), nu);
-  *J_fixed = value[best];
-  return DTP_OK;
+    std::vector<int64_t> value(reps.size());
+    std::vector<std::vector<int32_t>> nus(reps.size(), std::vector<int32_t>(I));
+    auto solve = [&](size_t j) {
+      int32_t hh[kMaxGroups];
+      for (int g = 0; g < G; ++g) hh[g] = table[(size_t)reps[j] * G + g];
+      std::vector<int64_t> M;
+      neuron_gain(G, I, L, Q_up, hh, nullptr, nullptr, false, &M);
+      balanced_assign_exact(I, L, M.data(), nus[j].data(), &value[j]);
+    };
+    const unsigned hw = std::max(1u, std::min(16u, std::thread::hardware_concurrency()));
+    std::vector<std::thread> pool;
+    for (unsigned t = 0; t < hw; ++t)
+      pool.emplace_back([&, t] {
+        for (size_t j = t; j < reps.size(); j += hw) solve(j);
+      });
+    for (auto& th : pool) th.join();
+    size_t best = 0;  // first partition (lexicographic) attaining the maximum
+    for (size_t j = 1; j < reps.size(); ++j)
+      if (value[j] > value[best]) best = j;
+    for (int g = 0; g < G; ++g) h[g] = table[(size_t)reps[best] * G + g];
+    std::copy(nus[best].begin(), nus[best].end(), nu);
+    *J_fixed = value[best];
+    return DTP_OK;
+  });
 }
 
 }  // extern "C"

@@ -1325,170 +1325,186 @@ dtp_status accumulate(dtp_layer L, const void* x, const void* attn, const void* 
 extern "C" {
 
 dtp_status dtp_layer_create(const dtp_layer_desc* desc, dtp_layer* out) {
-  clear_error();
-  DTP_CHECK(desc != nullptr && out != nullptr, DTP_ERR_INVALID_ARG, "desc or out is NULL");
-  const dtp_layer_desc& d = *desc;
-  DTP_CHECK(d.d_model > 0 && d.n_neurons > 0 && d.n_q_heads > 0 && d.n_kv_groups > 0 &&
-                d.head_dim > 0,
-            DTP_ERR_INVALID_ARG, "every size must be positive (d=%d I=%d H=%d G=%d dh=%d)",
-            d.d_model, d.n_neurons, d.n_q_heads, d.n_kv_groups, d.head_dim);
-  DTP_CHECK(d.n_q_heads % d.n_kv_groups == 0, DTP_ERR_INVALID_ARG,
-            "H=%d is not a multiple of G=%d", d.n_q_heads, d.n_kv_groups);
-  DTP_CHECK(d.n_kv_groups <= kMaxAffinityGroups, DTP_ERR_UNSUPPORTED, "G=%d exceeds %d",
-            d.n_kv_groups, kMaxAffinityGroups);
-  DTP_CHECK(d.head_dim % 16 == 0, DTP_ERR_INVALID_ARG, "head_dim=%d is not a multiple of 16",
-            d.head_dim);
-  DTP_CHECK(d.d_model % 16 == 0, DTP_ERR_INVALID_ARG, "d_model=%d is not a multiple of 16",
-            d.d_model);
-  DTP_CHECK(d.d_model <= 65536 && d.n_neurons <= (1 << 20) &&
-                (int64_t)d.n_q_heads * d.head_dim <= 65536,
-            DTP_ERR_UNSUPPORTED, "shape too large (d <= 65536, I <= 2^20, H*dh <= 65536)");
-  DTP_CHECK(std::isfinite(d.rms_eps) && d.rms_eps >= 0.0f, DTP_ERR_INVALID_ARG,
-            "rms_eps=%g must be finite and >= 0", (double)d.rms_eps);
-  DTP_CHECK(d.dtype == DTP_BF16 || d.dtype == DTP_F32, DTP_ERR_UNSUPPORTED, "dtype %d",
-            d.dtype);
-  dtp_layer L = new (std::nothrow) dtp_layer_s();
-  DTP_CHECK(L != nullptr, DTP_ERR_NO_MEMORY, "host allocation failed");
-  L->desc = d;
-  hipError_t e = hipGetDevice(&L->device);
-  L->n_tiles = (d.n_neurons + 2 * kBN - 1) / (2 * kBN) * 2;  // even: a block may span two tiles
-  L->I_pad = L->n_tiles * kBN;
-  const int64_t HD = (int64_t)d.n_q_heads * d.head_dim;
-  const size_t rows = (size_t)L->n_tiles * kCols;
-  if (d.dtype == DTP_BF16) {
-    L->Kt = d.d_model + (int)HD;
-    // Element offsets inside the tiled slice stay below 2^30.
-    L->tile_slice = std::max<int64_t>(256, std::min<int64_t>(kTileTokens, ((int64_t)1 << 30) / L->Kt) / 256 * 256);
-    if (e == hipSuccess) e = hipMalloc(&L->w, 2 * rows * L->Kt);
-    if (e == hipSuccess) e = hipMalloc(&L->woT, 2 * (size_t)HD * d.d_model);
-    if (e == hipSuccess) e = hipMalloc(&L->xt, 2 * (size_t)L->tile_slice * L->Kt);
-  } else {
-    L->Kt = d.d_model;
-    if (e == hipSuccess) e = hipMalloc(&L->w, 4 * rows * d.d_model);
-    if (e == hipSuccess) e = hipMalloc(&L->fold32, 4 * (size_t)HD * 2 * d.n_neurons);
-  }
-  if (e == hipSuccess) e = hipMalloc(&L->nd, 4 * (size_t)L->I_pad);
-  if (e == hipSuccess) e = hipMalloc(&L->rinv, 4 * (size_t)kSliceTokens);
-  if (e == hipSuccess)
-    e = hipMalloc(&L->partial, 4 * (size_t)kMaxSplits * (d.n_kv_groups + 1) * L->I_pad);
-  if (e == hipSuccess) e = hipMalloc(&L->rinv_next, 4 * (size_t)kSliceTokens);
-  if (e != hipSuccess) {
-    layer_free(L);
-    return fail(e == hipErrorOutOfMemory ? DTP_ERR_NO_MEMORY : DTP_ERR_HIP,
-                "layer allocation failed: %s", hipGetErrorString(e));
-  }
-  *out = L;
-  return DTP_OK;
+  return guarded([&]() -> dtp_status {
+    clear_error();
+    DTP_CHECK(desc != nullptr && out != nullptr, DTP_ERR_INVALID_ARG, "desc or out is NULL");
+    const dtp_layer_desc& d = *desc;
+    DTP_CHECK(d.d_model > 0 && d.n_neurons > 0 && d.n_q_heads > 0 && d.n_kv_groups > 0 &&
+                  d.head_dim > 0,
+              DTP_ERR_INVALID_ARG, "every size must be positive (d=%d I=%d H=%d G=%d dh=%d)",
+              d.d_model, d.n_neurons, d.n_q_heads, d.n_kv_groups, d.head_dim);
+    DTP_CHECK(d.n_q_heads % d.n_kv_groups == 0, DTP_ERR_INVALID_ARG,
+              "H=%d is not a multiple of G=%d", d.n_q_heads, d.n_kv_groups);
+    DTP_CHECK(d.n_kv_groups <= kMaxAffinityGroups, DTP_ERR_UNSUPPORTED, "G=%d exceeds %d",
+              d.n_kv_groups, kMaxAffinityGroups);
+    DTP_CHECK(d.head_dim % 16 == 0, DTP_ERR_INVALID_ARG, "head_dim=%d is not a multiple of 16",
+              d.head_dim);
+    DTP_CHECK(d.d_model % 16 == 0, DTP_ERR_INVALID_ARG, "d_model=%d is not a multiple of 16",
+              d.d_model);
+    DTP_CHECK(d.d_model <= 65536 && d.n_neurons <= (1 << 20) &&
+                  (int64_t)d.n_q_heads * d.head_dim <= 65536,
+              DTP_ERR_UNSUPPORTED, "shape too large (d <= 65536, I <= 2^20, H*dh <= 65536)");
+    DTP_CHECK(std::isfinite(d.rms_eps) && d.rms_eps >= 0.0f, DTP_ERR_INVALID_ARG,
+              "rms_eps=%g must be finite and >= 0", (double)d.rms_eps);
+    DTP_CHECK(d.dtype == DTP_BF16 || d.dtype == DTP_F32, DTP_ERR_UNSUPPORTED, "dtype %d",
+              d.dtype);
+    dtp_layer L = new (std::nothrow) dtp_layer_s();
+    DTP_CHECK(L != nullptr, DTP_ERR_NO_MEMORY, "host allocation failed");
+    L->desc = d;
+    hipError_t e = hipGetDevice(&L->device);
+    L->n_tiles = (d.n_neurons + 2 * kBN - 1) / (2 * kBN) * 2;  // even: a block may span two tiles
+    L->I_pad = L->n_tiles * kBN;
+    const int64_t HD = (int64_t)d.n_q_heads * d.head_dim;
+    const size_t rows = (size_t)L->n_tiles * kCols;
+    if (d.dtype == DTP_BF16) {
+      L->Kt = d.d_model + (int)HD;
+      // Element offsets inside the tiled slice stay below 2^30.
+      L->tile_slice = std::max<int64_t>(256, std::min<int64_t>(kTileTokens, ((int64_t)1 << 30) / L->Kt) / 256 * 256);
+      if (e == hipSuccess) e = hipMalloc(&L->w, 2 * rows * L->Kt);
+      if (e == hipSuccess) e = hipMalloc(&L->woT, 2 * (size_t)HD * d.d_model);
+      if (e == hipSuccess) e = hipMalloc(&L->xt, 2 * (size_t)L->tile_slice * L->Kt);
+    } else {
+      L->Kt = d.d_model;
+      if (e == hipSuccess) e = hipMalloc(&L->w, 4 * rows * d.d_model);
+      if (e == hipSuccess) e = hipMalloc(&L->fold32, 4 * (size_t)HD * 2 * d.n_neurons);
+    }
+    if (e == hipSuccess) e = hipMalloc(&L->nd, 4 * (size_t)L->I_pad);
+    if (e == hipSuccess) e = hipMalloc(&L->rinv, 4 * (size_t)kSliceTokens);
+    if (e == hipSuccess)
+      e = hipMalloc(&L->partial, 4 * (size_t)kMaxSplits * (d.n_kv_groups + 1) * L->I_pad);
+    if (e == hipSuccess) e = hipMalloc(&L->rinv_next, 4 * (size_t)kSliceTokens);
+    if (e != hipSuccess) {
+      layer_free(L);
+      return fail(e == hipErrorOutOfMemory ? DTP_ERR_NO_MEMORY : DTP_ERR_HIP,
+                  "layer allocation failed: %s", hipGetErrorString(e));
+    }
+    *out = L;
+    return DTP_OK;
+  });
 }
 
 dtp_status dtp_layer_destroy(dtp_layer layer) {
-  clear_error();
-  if (layer) layer_free(layer);
-  return DTP_OK;
+  return guarded([&]() -> dtp_status {
+    clear_error();
+    if (layer) layer_free(layer);
+    return DTP_OK;
+  });
 }
 
 dtp_status dtp_layer_set_weights(dtp_layer L, const void* w_o, const void* gamma,
                                  const void* w_gate, const void* w_up, const void* w_down,
                                  void* stream) {
-  clear_error();
-  DTP_CHECK(L != nullptr, DTP_ERR_INVALID_ARG, "layer is NULL");
-  DTP_CHECK(w_o && gamma && w_gate && w_up && w_down, DTP_ERR_INVALID_ARG,
-            "a weight pointer is NULL");
-  dtp_status st = check_device(L);
-  if (st != DTP_OK) return st;
-  hipStream_t s = (hipStream_t)stream;
-  const dtp_layer_desc& d = L->desc;
-  const int H = d.n_q_heads, dh = d.head_dim, HD = H * dh, I = d.n_neurons, dm = d.d_model;
-  const int64_t n = (int64_t)L->n_tiles * kCols * dm;
-  {
-    const size_t esz = d.dtype == DTP_BF16 ? 2 : 4;
-    const void* ptrs[5] = {w_o, gamma, w_gate, w_up, w_down};
-    const size_t elems[5] = {(size_t)dm * HD, (size_t)dm, (size_t)I * dm, (size_t)I * dm,
-                             (size_t)dm * I};
-    const char* names[5] = {"w_o", "gamma", "w_gate", "w_up", "w_down"};
-    for (int i = 0; i < 5; ++i)
-      if ((st = check_dev_buffer(ptrs[i], esz * elems[i], names[i])) != DTP_OK) return st;
-  }
-  if (d.dtype == DTP_BF16) {
-    if (aligned16(w_gate) && aligned16(w_up) && aligned16(gamma))
-      prep_gate_up_bf16x8_kernel<<<grid_for(n / 8, 256), 256, 0, s>>>(
-          (const uint16_t*)w_gate, (const uint16_t*)w_up, (const uint16_t*)gamma, I, dm,
-          L->n_tiles, L->Kt, (uint16_t*)L->w);
-    else
-      prep_gate_up_kernel<uint16_t><<<grid_for(n, 256), 256, 0, s>>>(
-          (const uint16_t*)w_gate, (const uint16_t*)w_up, (const uint16_t*)gamma, I, dm,
-          L->n_tiles, L->Kt, (uint16_t*)L->w);
-    DTP_HIP(hipGetLastError());
-    dim3 tg((HD + 31) / 32, (dm + 31) / 32);
-    transpose_kernel<<<tg, 256, 0, s>>>((const uint16_t*)w_o, dm, HD, (uint16_t*)L->woT);
-    DTP_HIP(hipGetLastError());
-    dim3 fg(L->n_tiles * kCols / kBM, (HD + kCols - 1) / kCols);
-    fold_kernel<<<fg, kThreads, 0, s>>>((uint16_t*)L->w, (const uint16_t*)L->woT, HD, dm, L->Kt);
-    DTP_HIP(hipGetLastError());
-    st = down_norms((const uint16_t*)w_down, L, s);
+  return guarded([&]() -> dtp_status {
+    clear_error();
+    DTP_CHECK(L != nullptr, DTP_ERR_INVALID_ARG, "layer is NULL");
+    DTP_CHECK(w_o && gamma && w_gate && w_up && w_down, DTP_ERR_INVALID_ARG,
+              "a weight pointer is NULL");
+    dtp_status st = check_device(L);
     if (st != DTP_OK) return st;
-  } else {
-    prep_gate_up_kernel<float><<<grid_for(n, 256), 256, 0, s>>>(
-        (const float*)w_gate, (const float*)w_up, (const float*)gamma, I, dm, L->n_tiles, dm,
-        (float*)L->w);
-    DTP_HIP(hipGetLastError());
-    const int64_t nf = (int64_t)H * 2 * I * dh;
-    fold_f32_kernel<<<grid_for(nf, 256), 256, 0, s>>>((const float*)w_o, (const float*)gamma,
-                                                       (const float*)w_gate, (const float*)w_up,
-                                                       dm, I, H, dh, L->fold32);
-    DTP_HIP(hipGetLastError());
-    st = down_norms((const float*)w_down, L, s);
-    if (st != DTP_OK) return st;
-  }
-  L->has_weights = true;
-  return DTP_OK;
+    hipStream_t s = (hipStream_t)stream;
+    const dtp_layer_desc& d = L->desc;
+    const int H = d.n_q_heads, dh = d.head_dim, HD = H * dh, I = d.n_neurons, dm = d.d_model;
+    const int64_t n = (int64_t)L->n_tiles * kCols * dm;
+    {
+      const size_t esz = d.dtype == DTP_BF16 ? 2 : 4;
+      const void* ptrs[5] = {w_o, gamma, w_gate, w_up, w_down};
+      const size_t elems[5] = {(size_t)dm * HD, (size_t)dm, (size_t)I * dm, (size_t)I * dm,
+                               (size_t)dm * I};
+      const char* names[5] = {"w_o", "gamma", "w_gate", "w_up", "w_down"};
+      for (int i = 0; i < 5; ++i)
+        if ((st = check_dev_buffer(ptrs[i], esz * elems[i], names[i])) != DTP_OK) return st;
+    }
+    if (d.dtype == DTP_BF16) {
+      if (aligned16(w_gate) && aligned16(w_up) && aligned16(gamma))
+        prep_gate_up_bf16x8_kernel<<<grid_for(n / 8, 256), 256, 0, s>>>(
+            (const uint16_t*)w_gate, (const uint16_t*)w_up, (const uint16_t*)gamma, I, dm,
+            L->n_tiles, L->Kt, (uint16_t*)L->w);
+      else
+        prep_gate_up_kernel<uint16_t><<<grid_for(n, 256), 256, 0, s>>>(
+            (const uint16_t*)w_gate, (const uint16_t*)w_up, (const uint16_t*)gamma, I, dm,
+            L->n_tiles, L->Kt, (uint16_t*)L->w);
+      DTP_HIP(hipGetLastError());
+      dim3 tg((HD + 31) / 32, (dm + 31) / 32);
+      transpose_kernel<<<tg, 256, 0, s>>>((const uint16_t*)w_o, dm, HD, (uint16_t*)L->woT);
+      DTP_HIP(hipGetLastError());
+      dim3 fg(L->n_tiles * kCols / kBM, (HD + kCols - 1) / kCols);
+      fold_kernel<<<fg, kThreads, 0, s>>>((uint16_t*)L->w, (const uint16_t*)L->woT, HD, dm, L->Kt);
+      DTP_HIP(hipGetLastError());
+      st = down_norms((const uint16_t*)w_down, L, s);
+      if (st != DTP_OK) return st;
+    } else {
+      prep_gate_up_kernel<float><<<grid_for(n, 256), 256, 0, s>>>(
+          (const float*)w_gate, (const float*)w_up, (const float*)gamma, I, dm, L->n_tiles, dm,
+          (float*)L->w);
+      DTP_HIP(hipGetLastError());
+      const int64_t nf = (int64_t)H * 2 * I * dh;
+      fold_f32_kernel<<<grid_for(nf, 256), 256, 0, s>>>((const float*)w_o, (const float*)gamma,
+                                                         (const float*)w_gate, (const float*)w_up,
+                                                         dm, I, H, dh, L->fold32);
+      DTP_HIP(hipGetLastError());
+      st = down_norms((const float*)w_down, L, s);
+      if (st != DTP_OK) return st;
+    }
+    L->has_weights = true;
+    return DTP_OK;
+  });
 }
 
 dtp_status dtp_affinity_accumulate(dtp_layer L, const void* x, const void* attn, int64_t n_tokens,
                                    float* A, void* stream) {
-  clear_error();
-  return dtp::accumulate(L, x, attn, nullptr, 0.0f, n_tokens, A, nullptr, false, stream);
+  return guarded([&]() -> dtp_status {
+    clear_error();
+    return dtp::accumulate(L, x, attn, nullptr, 0.0f, n_tokens, A, nullptr, false, stream);
+  });
 }
 
 dtp_status dtp_affinity_accumulate_add(dtp_layer L, const void* x, const void* attn,
                                        int64_t n_tokens, float* A, void* stream) {
-  clear_error();
-  return dtp::accumulate(L, x, attn, nullptr, 0.0f, n_tokens, A, nullptr, true, stream);
+  return guarded([&]() -> dtp_status {
+    clear_error();
+    return dtp::accumulate(L, x, attn, nullptr, 0.0f, n_tokens, A, nullptr, true, stream);
+  });
 }
 
 dtp_status dtp_affinity_accumulate_down(dtp_layer L, const void* x, const void* attn,
                                         const void* x_next, float rms_eps_next, int64_t n_tokens,
                                         float* A, float* s_down, void* stream) {
-  clear_error();
-  DTP_CHECK(x_next && s_down, DTP_ERR_INVALID_ARG, "x_next or s_down is NULL");
-  return dtp::accumulate(L, x, attn, x_next, rms_eps_next, n_tokens, A, s_down, false, stream);
+  return guarded([&]() -> dtp_status {
+    clear_error();
+    DTP_CHECK(x_next && s_down, DTP_ERR_INVALID_ARG, "x_next or s_down is NULL");
+    return dtp::accumulate(L, x, attn, x_next, rms_eps_next, n_tokens, A, s_down, false, stream);
+  });
 }
 
 dtp_status dtp_layer_profile(dtp_layer L, int32_t enable) {
-  clear_error();
-  DTP_CHECK(L != nullptr, DTP_ERR_INVALID_ARG, "layer is NULL");
-  L->profiling = enable != 0;
-  return DTP_OK;
+  return guarded([&]() -> dtp_status {
+    clear_error();
+    DTP_CHECK(L != nullptr, DTP_ERR_INVALID_ARG, "layer is NULL");
+    L->profiling = enable != 0;
+    return DTP_OK;
+  });
 }
 
 dtp_status dtp_layer_profile_read(dtp_layer L, double* total_ms, int64_t* launches) {
-  clear_error();
-  DTP_CHECK(L != nullptr && total_ms && launches, DTP_ERR_INVALID_ARG, "NULL argument");
-  double sum = 0.0;
-  for (auto& e : L->events) {
-    DTP_HIP(hipEventSynchronize(e.second));
-    float ms = 0.0f;
-    DTP_HIP(hipEventElapsedTime(&ms, e.first, e.second));
-    sum += ms;
-  }
-  *total_ms = sum;
-  *launches = (int64_t)L->events.size();
-  for (auto& e : L->events) {
-    (void)hipEventDestroy(e.first);
-    (void)hipEventDestroy(e.second);
-  }
-  L->events.clear();
-  return DTP_OK;
+  return guarded([&]() -> dtp_status {
+    clear_error();
+    DTP_CHECK(L != nullptr && total_ms && launches, DTP_ERR_INVALID_ARG, "NULL argument");
+    double sum = 0.0;
+    for (auto& e : L->events) {
+      DTP_HIP(hipEventSynchronize(e.second));
+      float ms = 0.0f;
+      DTP_HIP(hipEventElapsedTime(&ms, e.first, e.second));
+      sum += ms;
+    }
+    *total_ms = sum;
+    *launches = (int64_t)L->events.size();
+    for (auto& e : L->events) {
+      (void)hipEventDestroy(e.first);
+      (void)hipEventDestroy(e.second);
+    }
+    L->events.clear();
+    return DTP_OK;
+  });
 }
 
 }  // extern "C"

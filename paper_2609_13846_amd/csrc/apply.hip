@@ -81,93 +81,97 @@ extern "C" {
 
 dtp_status dtp_layout_orders(int32_t G, int32_t I, int32_t L, const int32_t* h, const int32_t* nu,
                              int32_t* group_order, int32_t* neuron_order) {
-  clear_error();
-  DTP_CHECK(G > 0 && I > 0 && L > 0 && G % L == 0 && I % L == 0, DTP_ERR_INVALID_ARG,
-            "G=%d and I=%d must be positive multiples of L=%d", G, I, L);
-  DTP_CHECK(h && nu && group_order && neuron_order, DTP_ERR_INVALID_ARG, "a pointer is NULL");
-  dtp_status st = check_assignment(h, G, L, "h");
-  if (st != DTP_OK) return st;
-  if ((st = check_assignment(nu, I, L, "nu")) != DTP_OK) return st;
-  orders(G, I, L, h, nu, group_order, neuron_order);
-  return DTP_OK;
+  return guarded([&]() -> dtp_status {
+    clear_error();
+    DTP_CHECK(G > 0 && I > 0 && L > 0 && G % L == 0 && I % L == 0, DTP_ERR_INVALID_ARG,
+              "G=%d and I=%d must be positive multiples of L=%d", G, I, L);
+    DTP_CHECK(h && nu && group_order && neuron_order, DTP_ERR_INVALID_ARG, "a pointer is NULL");
+    dtp_status st = check_assignment(h, G, L, "h");
+    if (st != DTP_OK) return st;
+    if ((st = check_assignment(nu, I, L, "nu")) != DTP_OK) return st;
+    orders(G, I, L, h, nu, group_order, neuron_order);
+    return DTP_OK;
+  });
 }
 
 dtp_status dtp_apply_layout(const dtp_layer_desc* desc, int32_t L, const int32_t* h,
                             const int32_t* nu, const void* const* src, void* const* dst,
                             void* stream) {
-  clear_error();
-  DTP_CHECK(desc && h && nu && src && dst, DTP_ERR_INVALID_ARG, "a pointer is NULL");
-  const dtp_layer_desc& d = *desc;
-  const int G = d.n_kv_groups, H = d.n_q_heads, dh = d.head_dim, I = d.n_neurons, dm = d.d_model;
-  DTP_CHECK(dm > 0 && I > 0 && H > 0 && G > 0 && dh > 0 && H % G == 0, DTP_ERR_INVALID_ARG,
-            "invalid layer shape (d=%d I=%d H=%d G=%d dh=%d)", dm, I, H, G, dh);
-  DTP_CHECK(L > 0 && G % L == 0 && I % L == 0, DTP_ERR_INVALID_ARG,
-            "G=%d and I=%d must be multiples of L=%d", G, I, L);
-  DTP_CHECK(d.dtype == DTP_BF16 || d.dtype == DTP_F32, DTP_ERR_UNSUPPORTED, "dtype %d", d.dtype);
-  const int esz = d.dtype == DTP_BF16 ? 2 : 4;
-  DTP_CHECK(((int64_t)dm * esz) % 16 == 0, DTP_ERR_INVALID_ARG,
-            "rows of d=%d elements must be a multiple of 16 bytes", dm);
-  for (int i = 0; i < 7; ++i) {
-    DTP_CHECK(src[i] && dst[i], DTP_ERR_INVALID_ARG, "weight %d is NULL", i);
-    DTP_CHECK(((uintptr_t)src[i] & 15u) == 0 && ((uintptr_t)dst[i] & 15u) == 0,
-              DTP_ERR_INVALID_ARG, "weight %d is not 16-byte aligned", i);
-    DTP_CHECK(src[i] != dst[i], DTP_ERR_INVALID_ARG, "weight %d: in-place permutation", i);
-  }
-  dtp_status st = check_assignment(h, G, L, "h");
-  if (st != DTP_OK) return st;
-  if ((st = check_assignment(nu, I, L, "nu")) != DTP_OK) return st;
-  {
-    const size_t hd = (size_t)H * dh, gd = (size_t)G * dh;
-    const size_t elems[7] = {hd * dm, gd * dm, gd * dm, (size_t)dm * hd, (size_t)I * dm,
-                             (size_t)I * dm, (size_t)dm * I};
-    const char* src_names[7] = {"src w_q", "src w_k", "src w_v", "src w_o", "src w_gate",
-                                "src w_up", "src w_down"};
-    const char* dst_names[7] = {"dst w_q", "dst w_k", "dst w_v", "dst w_o", "dst w_gate",
-                                "dst w_up", "dst w_down"};
+  return guarded([&]() -> dtp_status {
+    clear_error();
+    DTP_CHECK(desc && h && nu && src && dst, DTP_ERR_INVALID_ARG, "a pointer is NULL");
+    const dtp_layer_desc& d = *desc;
+    const int G = d.n_kv_groups, H = d.n_q_heads, dh = d.head_dim, I = d.n_neurons, dm = d.d_model;
+    DTP_CHECK(dm > 0 && I > 0 && H > 0 && G > 0 && dh > 0 && H % G == 0, DTP_ERR_INVALID_ARG,
+              "invalid layer shape (d=%d I=%d H=%d G=%d dh=%d)", dm, I, H, G, dh);
+    DTP_CHECK(L > 0 && G % L == 0 && I % L == 0, DTP_ERR_INVALID_ARG,
+              "G=%d and I=%d must be multiples of L=%d", G, I, L);
+    DTP_CHECK(d.dtype == DTP_BF16 || d.dtype == DTP_F32, DTP_ERR_UNSUPPORTED, "dtype %d", d.dtype);
+    const int esz = d.dtype == DTP_BF16 ? 2 : 4;
+    DTP_CHECK(((int64_t)dm * esz) % 16 == 0, DTP_ERR_INVALID_ARG,
+              "rows of d=%d elements must be a multiple of 16 bytes", dm);
     for (int i = 0; i < 7; ++i) {
-      if ((st = check_dev_buffer(src[i], esz * elems[i], src_names[i])) != DTP_OK) return st;
-      if ((st = check_dev_buffer(dst[i], esz * elems[i], dst_names[i])) != DTP_OK) return st;
+      DTP_CHECK(src[i] && dst[i], DTP_ERR_INVALID_ARG, "weight %d is NULL", i);
+      DTP_CHECK(((uintptr_t)src[i] & 15u) == 0 && ((uintptr_t)dst[i] & 15u) == 0,
+                DTP_ERR_INVALID_ARG, "weight %d is not 16-byte aligned", i);
+      DTP_CHECK(src[i] != dst[i], DTP_ERR_INVALID_ARG, "weight %d: in-place permutation", i);
     }
-  }
-  std::vector<int32_t> ord(G + I);
-  orders(G, I, L, h, nu, ord.data(), ord.data() + G);
-  hipStream_t s = (hipStream_t)stream;
-  int32_t* dord = nullptr;
-  DTP_HIP(hipMallocAsync((void**)&dord, sizeof(int32_t) * (G + I), s));
-  hipError_t e = hipMemcpyAsync(dord, ord.data(), sizeof(int32_t) * (G + I), hipMemcpyHostToDevice, s);
-  const int32_t* go = dord;
-  const int32_t* no = dord + G;
-  const int hpg = H / G;
-  const int64_t vr = (int64_t)dm * esz / 16;  // 16-byte vectors per row of d elements
-  auto rows = [&](int i, int64_t n_rows, int block, const int32_t* ord_dev) {
-    if (e != hipSuccess) return;
-    permute_rows_kernel<<<grid1(n_rows * vr), 256, 0, s>>>((const u32x4*)src[i], (u32x4*)dst[i],
-                                                           n_rows, vr, block, ord_dev);
-    e = hipGetLastError();
-  };
-  auto cols = [&](int i, int64_t n_cols, int block, const int32_t* ord_dev) {
-    if (e != hipSuccess) return;
-    if (esz == 2)
-      permute_cols_kernel<uint16_t><<<grid1((int64_t)dm * n_cols), 256, 0, s>>>(
-          (const uint16_t*)src[i], (uint16_t*)dst[i], dm, n_cols, block, ord_dev);
-    else
-      permute_cols_kernel<float><<<grid1((int64_t)dm * n_cols), 256, 0, s>>>(
-          (const float*)src[i], (float*)dst[i], dm, n_cols, block, ord_dev);
-    e = hipGetLastError();
-  };
-  rows(0, (int64_t)H * dh, hpg * dh, go);  // w_q: a group's query heads are one block
-  rows(1, (int64_t)G * dh, dh, go);        // w_k
-  rows(2, (int64_t)G * dh, dh, go);        // w_v
-  cols(3, (int64_t)H * dh, hpg * dh, go);  // w_o columns, like the q rows
-  rows(4, I, 1, no);                       // w_gate
-  rows(5, I, 1, no);                       // w_up
-  cols(6, I, 1, no);                       // w_down columns
-  const hipError_t ef = hipFreeAsync(dord, s);
-  DTP_HIP(e);
-  DTP_HIP(ef);
-  // The order upload reads `ord`, which dies on return.
-  DTP_HIP(hipStreamSynchronize(s));
-  return DTP_OK;
+    dtp_status st = check_assignment(h, G, L, "h");
+    if (st != DTP_OK) return st;
+    if ((st = check_assignment(nu, I, L, "nu")) != DTP_OK) return st;
+    {
+      const size_t hd = (size_t)H * dh, gd = (size_t)G * dh;
+      const size_t elems[7] = {hd * dm, gd * dm, gd * dm, (size_t)dm * hd, (size_t)I * dm,
+                               (size_t)I * dm, (size_t)dm * I};
+      const char* src_names[7] = {"src w_q", "src w_k", "src w_v", "src w_o", "src w_gate",
+                                  "src w_up", "src w_down"};
+      const char* dst_names[7] = {"dst w_q", "dst w_k", "dst w_v", "dst w_o", "dst w_gate",
+                                  "dst w_up", "dst w_down"};
+      for (int i = 0; i < 7; ++i) {
+        if ((st = check_dev_buffer(src[i], esz * elems[i], src_names[i])) != DTP_OK) return st;
+        if ((st = check_dev_buffer(dst[i], esz * elems[i], dst_names[i])) != DTP_OK) return st;
+      }
+    }
+    std::vector<int32_t> ord(G + I);
+    orders(G, I, L, h, nu, ord.data(), ord.data() + G);
+    hipStream_t s = (hipStream_t)stream;
+    int32_t* dord = nullptr;
+    DTP_HIP(hipMallocAsync((void**)&dord, sizeof(int32_t) * (G + I), s));
+    hipError_t e = hipMemcpyAsync(dord, ord.data(), sizeof(int32_t) * (G + I), hipMemcpyHostToDevice, s);
+    const int32_t* go = dord;
+    const int32_t* no = dord + G;
+    const int hpg = H / G;
+    const int64_t vr = (int64_t)dm * esz / 16;  // 16-byte vectors per row of d elements
+    auto rows = [&](int i, int64_t n_rows, int block, const int32_t* ord_dev) {
+      if (e != hipSuccess) return;
+      permute_rows_kernel<<<grid1(n_rows * vr), 256, 0, s>>>((const u32x4*)src[i], (u32x4*)dst[i],
+                                                             n_rows, vr, block, ord_dev);
+      e = hipGetLastError();
+    };
+    auto cols = [&](int i, int64_t n_cols, int block, const int32_t* ord_dev) {
+      if (e != hipSuccess) return;
+      if (esz == 2)
+        permute_cols_kernel<uint16_t><<<grid1((int64_t)dm * n_cols), 256, 0, s>>>(
+            (const uint16_t*)src[i], (uint16_t*)dst[i], dm, n_cols, block, ord_dev);
+      else
+        permute_cols_kernel<float><<<grid1((int64_t)dm * n_cols), 256, 0, s>>>(
+            (const float*)src[i], (float*)dst[i], dm, n_cols, block, ord_dev);
+      e = hipGetLastError();
+    };
+    rows(0, (int64_t)H * dh, hpg * dh, go);  // w_q: a group's query heads are one block
+    rows(1, (int64_t)G * dh, dh, go);        // w_k
+    rows(2, (int64_t)G * dh, dh, go);        // w_v
+    cols(3, (int64_t)H * dh, hpg * dh, go);  // w_o columns, like the q rows
+    rows(4, I, 1, no);                       // w_gate
+    rows(5, I, 1, no);                       // w_up
+    cols(6, I, 1, no);                       // w_down columns
+    const hipError_t ef = hipFreeAsync(dord, s);
+    DTP_HIP(e);
+    DTP_HIP(ef);
+    // The order upload reads `ord`, which dies on return.
+    DTP_HIP(hipStreamSynchronize(s));
+    return DTP_OK;
+  });
 }
 
 }  // extern "C"

@@ -262,9 +262,11 @@ dtp_status dtp_down_weights(int32_t d_model, int32_t n_neurons, int32_t n_q_head
                             int32_t n_kv_groups, int32_t head_dim, dtp_dtype dtype,
                             const void* w_q, const void* w_k, const void* w_v,
                             const void* gamma_next, const void* w_down, float* B, void* stream) {
-  clear_error();
-  return down_weights(d_model, n_neurons, n_q_heads, n_kv_groups, head_dim, dtype, w_q, w_k, w_v,
-                      gamma_next, w_down, B, false, stream);
+  return guarded([&]() -> dtp_status {
+    clear_error();
+    return down_weights(d_model, n_neurons, n_q_heads, n_kv_groups, head_dim, dtype, w_q, w_k, w_v,
+                        gamma_next, w_down, B, false, stream);
+  });
 }
 
 dtp_status dtp_down_weights_noalloc(int32_t d_model, int32_t n_neurons, int32_t n_q_heads,
@@ -272,27 +274,31 @@ dtp_status dtp_down_weights_noalloc(int32_t d_model, int32_t n_neurons, int32_t 
                                     const void* w_q, const void* w_k, const void* w_v,
                                     const void* gamma_next, const void* w_down, float* B,
                                     void* stream) {
-  clear_error();
-  return down_weights(d_model, n_neurons, n_q_heads, n_kv_groups, head_dim, dtype, w_q, w_k, w_v,
-                      gamma_next, w_down, B, true, stream);
+  return guarded([&]() -> dtp_status {
+    clear_error();
+    return down_weights(d_model, n_neurons, n_q_heads, n_kv_groups, head_dim, dtype, w_q, w_k, w_v,
+                        gamma_next, w_down, B, true, stream);
+  });
 }
 
 dtp_status dtp_down_affinity(int32_t n_neurons, int32_t n_kv_groups, const float* s_down,
                              const float* B, float* A_down, void* stream) {
-  clear_error();
-  DTP_CHECK(n_neurons > 0 && n_kv_groups > 0, DTP_ERR_INVALID_ARG, "I=%d and G=%d must be positive",
-            n_neurons, n_kv_groups);
-  DTP_CHECK(s_down && B && A_down, DTP_ERR_INVALID_ARG, "s_down, B or A_down is NULL");
-  hipStream_t s = (hipStream_t)stream;
-  const int64_t n = (int64_t)n_neurons * n_kv_groups;
-  dtp_status st;
-  if ((st = check_dev_buffer(s_down, sizeof(float) * (size_t)n_neurons, "s_down")) != DTP_OK ||
-      (st = check_dev_buffer(B, sizeof(float) * (size_t)n, "B")) != DTP_OK ||
-      (st = check_dev_buffer(A_down, sizeof(float) * (size_t)n, "A_down")) != DTP_OK)
-    return st;
-  down_combine_kernel<<<blocks_for(n, 256), 256, 0, s>>>(s_down, B, n_neurons, n_kv_groups, A_down);
-  DTP_HIP(hipGetLastError());
-  return DTP_OK;
+  return guarded([&]() -> dtp_status {
+    clear_error();
+    DTP_CHECK(n_neurons > 0 && n_kv_groups > 0, DTP_ERR_INVALID_ARG, "I=%d and G=%d must be positive",
+              n_neurons, n_kv_groups);
+    DTP_CHECK(s_down && B && A_down, DTP_ERR_INVALID_ARG, "s_down, B or A_down is NULL");
+    hipStream_t s = (hipStream_t)stream;
+    const int64_t n = (int64_t)n_neurons * n_kv_groups;
+    dtp_status st;
+    if ((st = check_dev_buffer(s_down, sizeof(float) * (size_t)n_neurons, "s_down")) != DTP_OK ||
+        (st = check_dev_buffer(B, sizeof(float) * (size_t)n, "B")) != DTP_OK ||
+        (st = check_dev_buffer(A_down, sizeof(float) * (size_t)n, "A_down")) != DTP_OK)
+      return st;
+    down_combine_kernel<<<blocks_for(n, 256), 256, 0, s>>>(s_down, B, n_neurons, n_kv_groups, A_down);
+    DTP_HIP(hipGetLastError());
+    return DTP_OK;
+  });
 }
 
 }  // extern "C"

@@ -4,6 +4,8 @@
 #include <hip/hip_runtime.h>
 
 #include <cstdint>
+#include <exception>
+#include <new>
 #include <string>
 #include <vector>
 
@@ -21,6 +23,21 @@ void clear_error();
 // entry point checks its device arguments this way before enqueueing work.  NULL is
 // accepted when `optional` (the argument is then unused).
 dtp_status check_dev_buffer(const void* p, size_t bytes, const char* what, bool optional = false);
+
+// Runs an entry point's body and turns any C++ exception (a host allocation, a thread the
+// neuron step could not start) into a status, so that nothing unwinds through the C ABI.
+template <typename F>
+dtp_status guarded(F&& body) noexcept {
+  try {
+    return body();
+  } catch (const std::bad_alloc&) {
+    return fail(DTP_ERR_NO_MEMORY, "host memory allocation failed");
+  } catch (const std::exception& e) {
+    return fail(DTP_ERR_NO_MEMORY, "host resource failure: %s", e.what());
+  } catch (...) {
+    return fail(DTP_ERR_NO_MEMORY, "unexpected host failure");
+  }
+}
 
 #define DTP_HIP(call)                                                                 \
   do {                                                                                \
