@@ -162,3 +162,49 @@ def test_layout_from_gpu_affinity_matches_oracle_objective():
     hs2, nus2, J2, _ = lay.coordinate_ascent([lay.encode(A_gpu)], None, L)
     np.testing.assert_array_equal(res["nu"][0], nus2[0])
     assert res["J_fixed"] == J2
+
+
+def test_concurrent_ascents_from_several_threads_match_serial():
+    """Four host threads, each with its own stream, run coordinate ascents at once (chains
+    with down edges, L = 2 and 4, and a call that fails on a degenerate matrix); every
+    result equals the same call run alone, and each failure reports its own error.  This
+    exercises the pinned staging pool, the stream-ordered scratch and the per-thread error
+    message under concurrency."""
+    import threading
+    announce("concurrent coordinate ascents, 4 threads")
+    rng = np.random.default_rng(77)
+    cases = []
+    for t in range(8):
+        N, L = (3, 4) if t % 2 else (2, 2)
+        G, I = 8, 512
+        Au = torch.from_numpy(rand_A(rng, (N, G, I))).cuda()
+        Ad = torch.from_numpy(rand_A(rng, (N - 1, I, G))).cuda()
+        cases.append((N, G, I, L, Au, Ad))
+    bad = torch.zeros(1, 8, 512, dtype=torch.float32, device="cuda")  # all zero: degenerate
+    torch.cuda.synchronize()
+    serial = [dtp.dtp_coordinate_ascent(*c) for c in cases]
+    results, errors = {}, {}
+
+    def worker(w):
+        stream = torch.cuda.Stream()
+        for rep in range(3):
+            for i in range(w, len(cases), 4):
+                results[(w, rep, i)] = dtp.dtp_coordinate_ascent(*cases[i], stream=stream)
+            try:
+                dtp.dtp_coordinate_ascent(1, 8, 512, 2, bad, stream=stream)
+                errors[(w, rep)] = None
+            except dtp.DtpError as e:
+                errors[(w, rep)] = e.status
+
+    threads = [threading.Thread(target=worker, args=(w,)) for w in range(4)]
+    for th in threads:
+        th.start()
+    for th in threads:
+        th.join()
+    assert len(results) == 3 * len(cases)
+    for (w, rep, i), res in results.items():
+        ref = serial[i]
+        np.testing.assert_array_equal(res["h"], ref["h"])
+        np.testing.assert_array_equal(res["nu"], ref["nu"])
+        assert res["J_fixed"] == ref["J_fixed"] and res["sweeps"] == ref["sweeps"]
+    assert all(s == dtp.DTP_ERR_DEGENERATE for s in errors.values()) and len(errors) == 12
