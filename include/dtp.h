@@ -23,6 +23,11 @@
  *     caller's responsibility.
  *   - `stream` is a hipStream_t (NULL = the default stream).  GPU work is enqueued on it
  *     asynchronously; functions that return host results synchronise that stream first.
+ *   - Host threads may call the library concurrently, each with its own stream: calls on
+ *     different layers, and the functions that take no layer, keep no shared mutable
+ *     state (their scratch comes per call from the stream-ordered allocator).  Calls on
+ *     one dtp_layer share its workspace and must be ordered by the caller (one stream,
+ *     or synchronised); so must overlapping calls of dtp_down_weights_noalloc on a device.
  *   - Weights use the PyTorch nn.Linear layout [out_features, in_features].
  *   - bf16 tensors are IEEE bfloat16 bit patterns (uint16); f32 tensors are float.
  */

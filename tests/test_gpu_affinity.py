@@ -241,3 +241,45 @@ def test_affinity_full_workload_sampled_neurons(name):
         hp.assert_affinity_close(A.cpu().numpy()[:, cols], ref)
     finally:
         dtp.dtp_layer_destroy(layer)
+
+
+def test_two_layers_accumulated_from_two_threads_match_serial():
+    """Two layers (their own workspaces), each fed from its own host thread and stream at
+    the same time, give exactly what each gives alone."""
+    import threading
+
+    import torch
+    announce("two layers accumulated concurrently from two threads")
+    wl = synth.WORKLOADS["qwen3-0.6b-layer"]
+    data = []
+    for layer_idx in range(2):
+        w = synth.host_weights(wl, layer_idx)
+        x, a = synth.host_tokens(wl, layer_idx, w, 3000)
+        data.append((w, x, a))
+    serial = [hp.gpu_affinity(wl, w, x, a) for (w, x, a) in data]
+    layers, inputs, outs = [], [], []
+    try:
+        for (w, x, a) in data:
+            layer = hp.layer_for(wl)
+            layers.append(layer)
+            dtp.dtp_layer_set_weights(layer, *(hp.torch_dev(v) for v in (w.w_o, w.gamma, w.w_gate, w.w_up, w.w_down)))
+            inputs.append((hp.torch_dev(x), hp.torch_dev(a)))
+            outs.append(torch.zeros(wl.n_kv_groups, wl.n_neurons, dtype=torch.float32, device="cuda"))
+        torch.cuda.synchronize()
+
+        def worker(i):
+            stream = torch.cuda.Stream()
+            for _ in range(3):
+                dtp.dtp_affinity_accumulate(layers[i], inputs[i][0], inputs[i][1], 3000, outs[i], stream=stream)
+            stream.synchronize()
+
+        threads = [threading.Thread(target=worker, args=(i,)) for i in range(2)]
+        for th in threads:
+            th.start()
+        for th in threads:
+            th.join()
+        for i in range(2):  # three accumulations of the same tokens: 3x the single pass
+            np.testing.assert_allclose(outs[i].cpu().numpy(), 3 * serial[i], rtol=1e-6)
+    finally:
+        for layer in layers:
+            dtp.dtp_layer_destroy(layer)
