@@ -192,31 +192,63 @@ __global__ void fold_f32_kernel(const float* __restrict__ w_o, const float* __re
   }
 }
 
-// nd[k] = sum_j w_down[j][k]^2 in two passes: part[c][k] sums the rows of chunk c (one
-// thread per chunk and column, coalesced across columns), then the chunks are added in order.
-template <typename T>
+// nd[k] = sum_j w_down[j][k]^2 in two passes: part[c][k] sums the rows of chunk c in row
+// order, then the chunks are added in order.  A thread of the first pass takes 8 adjacent
+// columns of its chunk, one 16-byte load per row where the rows allow it (VEC), so each
+// load carries 8 columns and a thread's rows are in flight together.
+template <typename T, bool VEC>
 __global__ void __launch_bounds__(256)
 down_norm_part_kernel(const T* __restrict__ w_down, int d, int I, int chunk_rows,
                       float* __restrict__ part) {
-  const int k = blockIdx.x * 256 + threadIdx.x;
+  const int k0 = 8 * (blockIdx.x * 256 + threadIdx.x);
   const int c = blockIdx.y;
-  if (k >= I) return;
+  if (k0 >= I) return;
   const int j1 = min(d, (c + 1) * chunk_rows);
-  float s = 0.0f;
-  for (int j = c * chunk_rows; j < j1; ++j) {
-    const float v = load_f32(w_down, (int64_t)j * I + k);
-    s = fmaf(v, v, s);
+  float s[8] = {};
+  if constexpr (VEC) {  // I % 8 == 0 and 16-byte aligned rows
+#pragma unroll 4
+    for (int j = c * chunk_rows; j < j1; ++j) {
+      const T* row = w_down + (int64_t)j * I + k0;
+      if constexpr (sizeof(T) == 2) {
+        const u32x4 v = *reinterpret_cast<const u32x4*>(row);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const float lo = __uint_as_float(v[e] << 16), hi = __uint_as_float(v[e] & 0xffff0000u);
+          s[2 * e] = fmaf(lo, lo, s[2 * e]);
+          s[2 * e + 1] = fmaf(hi, hi, s[2 * e + 1]);
+        }
+      } else {
+        const float4 a = *reinterpret_cast<const float4*>(row);
+        const float4 b = *reinterpret_cast<const float4*>(row + 4);
+        const float v[8] = {a.x, a.y, a.z, a.w, b.x, b.y, b.z, b.w};
+#pragma unroll
+        for (int e = 0; e < 8; ++e) s[e] = fmaf(v[e], v[e], s[e]);
+      }
+    }
+  } else {
+    for (int j = c * chunk_rows; j < j1; ++j)
+#pragma unroll
+      for (int e = 0; e < 8; ++e)
+        if (k0 + e < I) {
+          const float v = load_f32(w_down, (int64_t)j * I + k0 + e);
+          s[e] = fmaf(v, v, s[e]);
+        }
   }
-  part[(int64_t)c * I + k] = s;
+#pragma unroll
+  for (int e = 0; e < 8; ++e)
+    if (k0 + e < I) part[(int64_t)c * I + k0 + e] = s[e];
 }
 
-__global__ void down_norm_sum_kernel(const float* __restrict__ part, int chunks, int I, int I_pad,
-                                     float* __restrict__ nd) {
+__global__ void __launch_bounds__(64)
+down_norm_sum_kernel(const float* __restrict__ part, int chunks, int I, int I_pad,
+                     float* __restrict__ nd) {
   const int k = blockIdx.x * blockDim.x + threadIdx.x;
   if (k >= I_pad) return;
   double t = 0.0;
-  if (k < I)
+  if (k < I) {
+#pragma unroll 8
     for (int c = 0; c < chunks; ++c) t += (double)part[(int64_t)c * I + k];
+  }
   nd[k] = (float)t;
 }
 
@@ -1154,11 +1186,16 @@ dtp_status down_norms(const T* w_down, dtp_layer L, hipStream_t s) {
   int chunk_rows = 32;
   while ((int64_t)((d.d_model + chunk_rows - 1) / chunk_rows) * d.n_neurons > cap) chunk_rows *= 2;
   const int chunks = (d.d_model + chunk_rows - 1) / chunk_rows;
-  down_norm_part_kernel<T><<<dim3((d.n_neurons + 255) / 256, chunks), 256, 0, s>>>(
-      w_down, d.d_model, d.n_neurons, chunk_rows, L->partial);
+  const dim3 grid((d.n_neurons + 8 * 256 - 1) / (8 * 256), chunks);
+  if (d.n_neurons % 8 == 0 && aligned16(w_down))
+    down_norm_part_kernel<T, true><<<grid, 256, 0, s>>>(w_down, d.d_model, d.n_neurons, chunk_rows,
+                                                        L->partial);
+  else
+    down_norm_part_kernel<T, false><<<grid, 256, 0, s>>>(w_down, d.d_model, d.n_neurons, chunk_rows,
+                                                         L->partial);
   DTP_HIP(hipGetLastError());
-  down_norm_sum_kernel<<<(L->I_pad + 255) / 256, 256, 0, s>>>(L->partial, chunks, d.n_neurons,
-                                                               L->I_pad, L->nd);
+  down_norm_sum_kernel<<<(L->I_pad + 63) / 64, 64, 0, s>>>(L->partial, chunks, d.n_neurons, L->I_pad,
+                                                           L->nd);
   DTP_HIP(hipGetLastError());
   return DTP_OK;
 }

@@ -153,9 +153,11 @@ encode_div_kernel(int nup, int64_t n, const EncodeStats* st, int64_t* Q_up, int6
 }
 
 unsigned blocks_for(int64_t n) {
-  // About 16 entries per thread, and at most 65535 blocks: a thread then sums at most
-  // 2^30 / (65535 * 256) + 1 = 65 codes below 2^41 each.
-  const int64_t b = (n + kEncThreads * 16 - 1) / (kEncThreads * 16);
+  // About 4 entries per thread (a layer's G x I matrix then spreads over tens of CUs
+  // instead of a few, whose threads would wait on their loads one after another), and at
+  // most 65535 blocks: a thread then sums at most 2^30 / (65535 * 256) + 1 = 65 codes
+  // below 2^41 each.
+  const int64_t b = (n + kEncThreads * 4 - 1) / (kEncThreads * 4);
   return (unsigned)std::max<int64_t>(1, std::min<int64_t>(b, 65535));
 }
 

@@ -7,7 +7,7 @@
 // All quantities are int64 fixed-point codes, so sums are exact in any order.
 //
 // Kernels (all over N layers at once):
-//   head_gain_kernel      one block per (layer, group): C[g, :] by a block reduction
+//   head_gain_kernel      one block per (layer, group): C[g, :] in per-device LDS bins
 //   partition_score_kernel one wavefront per (layer, partition): lane g adds C[g, h(g)]
 //   best_partition_kernel one block per layer: best score, lowest rank on ties
 #include "dtp_internal.h"
@@ -17,7 +17,6 @@ namespace dtp {
 namespace {
 
 constexpr int kGainThreads = 256;
-constexpr int kMaxDevices = 64;
 
 __device__ inline int64_t wave_sum_i64(int64_t v) {
   for (int off = 32; off > 0; off >>= 1) {
@@ -28,35 +27,50 @@ __device__ inline int64_t wave_sum_i64(int64_t v) {
   return v;
 }
 
+// At most kMaxGainDevices devices: a balanced layout over L devices has at least L!
+// labelled partitions (G is a multiple of L), and 11! is beyond what the scoring accepts.
+constexpr int kMaxGainDevices = 10;
+static_assert(39916800 > kMaxPartitions, "11 devices would need more than 10 device sums");
+
+// C[g, :] of one (layer, group) in one pass over the neurons: each lane keeps one register
+// sum per device (DEV >= L of them, selects rather than a branch on the device index, so
+// a thread's loads of successive neurons are in flight together), then each sum is added
+// across the wavefront and one lane per wavefront adds it to the block's LDS bin.
+// Integer sums: exact in any order.  A device index outside [0, L) adds to no sum.
+template <int DEV>
 __global__ void __launch_bounds__(kGainThreads)
 head_gain_kernel(const int64_t* __restrict__ Q_up, const int32_t* __restrict__ nu,
                  const int64_t* __restrict__ Q_down, const int32_t* __restrict__ nu_down,
                  int G, int I, int L, int64_t* __restrict__ C) {
-  __shared__ int64_t part[kGainThreads / 64][kMaxDevices];
+  __shared__ unsigned long long bins[DEV];
   const int layer = blockIdx.x / G;
   const int g = blockIdx.x % G;
-  const int lane = threadIdx.x & 63;
-  const int wave = threadIdx.x >> 6;
+  if (threadIdx.x < DEV) bins[threadIdx.x] = 0ull;
+  __syncthreads();
   const int64_t* qu = Q_up + ((size_t)layer * G + g) * I;
   const int32_t* nl = nu + (size_t)layer * I;
   const bool down = Q_down != nullptr && layer > 0;
   const int64_t* qd = down ? Q_down + (size_t)(layer - 1) * I * G : nullptr;
   const int32_t* nd = down ? nu_down + (size_t)(layer - 1) * I : nullptr;
-  for (int l = 0; l < L; ++l) {
-    int64_t acc = 0;
-    for (int k = threadIdx.x; k < I; k += kGainThreads) {
-      if (nl[k] == l) acc += qu[k];
-      if (down && nd[k] == l) acc += qd[(size_t)k * G + g];
-    }
-    acc = wave_sum_i64(acc);
-    if (lane == 0) part[wave][l] = acc;
+  int64_t sum[DEV] = {};
+  auto add = [&](int l, int64_t v) __attribute__((always_inline)) {
+#pragma unroll
+    for (int j = 0; j < DEV; ++j) sum[j] += l == j ? v : 0;
+  };
+#pragma unroll 4
+  for (int k = threadIdx.x; k < I; k += kGainThreads) add(nl[k], qu[k]);
+  if (down) {
+#pragma unroll 4
+    for (int k = threadIdx.x; k < I; k += kGainThreads) add(nd[k], qd[(size_t)k * G + g]);
+  }
+#pragma unroll
+  for (int j = 0; j < DEV; ++j) {
+    const int64_t t = wave_sum_i64(sum[j]);
+    if ((threadIdx.x & 63) == 0) atomicAdd(&bins[j], (unsigned long long)t);
   }
   __syncthreads();
-  for (int l = threadIdx.x; l < L; l += kGainThreads) {
-    int64_t s = 0;
-    for (int w = 0; w < kGainThreads / 64; ++w) s += part[w][l];
-    C[((size_t)layer * G + g) * L + l] = s;
-  }
+  for (int l = threadIdx.x; l < L; l += kGainThreads)
+    C[((size_t)layer * G + g) * L + l] = (int64_t)bins[l];
 }
 
 // One wavefront per (layer, partition); lanes index KV groups (G <= 64).
@@ -151,10 +165,18 @@ void score_workspace_destroy(ScoreWorkspace* ws) {
 dtp_status launch_partition_scores(const ScoreWorkspace& ws, const int64_t* Q_up,
                                    const int32_t* nu, const int64_t* Q_down,
                                    const int32_t* nu_down, int minimise, hipStream_t stream) {
-  DTP_CHECK(ws.L <= kMaxDevices && ws.G <= kMaxGroups, DTP_ERR_UNSUPPORTED,
-            "partition scoring supports G <= %d and L <= %d", kMaxGroups, kMaxDevices);
-  head_gain_kernel<<<ws.N * ws.G, kGainThreads, 0, stream>>>(Q_up, nu, Q_down, nu_down, ws.G,
-                                                             ws.I, ws.L, ws.C);
+  DTP_CHECK(ws.L <= kMaxGainDevices && ws.G <= kMaxGroups, DTP_ERR_UNSUPPORTED,
+            "partition scoring supports G <= %d and L <= %d", kMaxGroups, kMaxGainDevices);
+  const unsigned gain_blocks = (unsigned)(ws.N * ws.G);
+  if (ws.L <= 2)
+    head_gain_kernel<2><<<gain_blocks, kGainThreads, 0, stream>>>(Q_up, nu, Q_down, nu_down, ws.G,
+                                                                  ws.I, ws.L, ws.C);
+  else if (ws.L <= 4)
+    head_gain_kernel<4><<<gain_blocks, kGainThreads, 0, stream>>>(Q_up, nu, Q_down, nu_down, ws.G,
+                                                                  ws.I, ws.L, ws.C);
+  else
+    head_gain_kernel<kMaxGainDevices><<<gain_blocks, kGainThreads, 0, stream>>>(
+        Q_up, nu, Q_down, nu_down, ws.G, ws.I, ws.L, ws.C);
   DTP_HIP(hipGetLastError());
   const int64_t waves = (int64_t)ws.N * ws.P;
   const int64_t blocks = (waves + 3) / 4;
