@@ -15,9 +15,11 @@ own time limit, writing CSV output (no database files):
   ``v_mfma_f32_16x16x32_bf16``, 32 per ``32x32x16``), GRBM_GUI_ACTIVE the GPU cycles of each
   of the 8 XCDs, so the MFMA busy fraction is MFMA_BUSY / (GRBM_GUI_ACTIVE / 8 * 1024 SIMDs)
   and GRBM_GUI_ACTIVE / 8 over the launch's duration is the clock it ran at;
-* ``stall``: ``--kernel-trace`` with the SQ counters of where a wave's cycles go: issuing
-  VALU (MFMAs included), LDS and scalar instructions, waiting at ``s_waitcnt`` (any
-  counter, and LDS alone), all over the wave cycles (SQ_WAVE_CYCLES, same units).
+* ``stall``: ``--kernel-trace`` with the SQ counters of where a wave's cycles go, all over
+  the wave cycles (SQ_WAVE_CYCLES, same units): issuing an instruction (VALU with the
+  MFMAs, LDS and scalar apart), ready with an instruction that its unit does not take yet
+  (SQ_WAIT_INST_ANY, and LDS instructions alone), and waiting at ``s_waitcnt`` or a
+  barrier (SQ_WAIT_ANY).  The three states cover the wave cycles.
 
 ``summarize`` writes a markdown summary of the kernel trace and the traffic of the
 affinity kernel (bytes per launch, counter scales applied) to ``profiles/``, plus the
@@ -188,8 +190,8 @@ def summarize(d: str, profiles: str, workload: str, bench_cmd: str) -> None:
                                              ("lds_issue", "SQ_ACTIVE_INST_LDS"),
                                              ("scalar_issue", "SQ_ACTIVE_INST_SCA"),
                                              ("any_issue", "SQ_ACTIVE_INST_ANY"),
-                                             ("waitcnt", "SQ_WAIT_INST_ANY"),
-                                             ("waitcnt_lds", "SQ_WAIT_INST_LDS"),
+                                             ("issue_wait", "SQ_WAIT_INST_ANY"),
+                                             ("issue_wait_lds", "SQ_WAIT_INST_LDS"),
                                              ("wait_any", "SQ_WAIT_ANY"))}
         lines += ["", "## Where a wave's cycles go (--pmc, one pass)", "",
                   f"Counters: {', '.join(STALL_COUNTERS)}; each as a share of SQ_WAVE_CYCLES "
@@ -197,8 +199,12 @@ def summarize(d: str, profiles: str, workload: str, bench_cmd: str) -> None:
                   f"- issuing VALU instructions (MFMAs included): {stall['valu_issue']:.1%}",
                   f"- issuing LDS instructions: {stall['lds_issue']:.1%}; scalar: {stall['scalar_issue']:.1%}; "
                   f"any: {stall['any_issue']:.1%}",
-                  f"- waiting at s_waitcnt: {stall['waitcnt']:.1%} (on LDS alone: {stall['waitcnt_lds']:.1%})",
-                  f"- waiting for anything (SQ_WAIT_ANY): {stall['wait_any']:.1%}"]
+                  f"- ready but not issued (SQ_WAIT_INST_ANY; an instruction waiting for its unit, "
+                  f"e.g. behind the other wave's MFMA): {stall['issue_wait']:.1%} "
+                  f"(LDS instructions: {stall['issue_wait_lds']:.1%})",
+                  f"- waiting at s_waitcnt or a barrier (SQ_WAIT_ANY): {stall['wait_any']:.1%}",
+                  f"- the three states (issuing, ready, waiting) add to "
+                  f"{stall['any_issue'] + stall['issue_wait'] + stall['wait_any']:.1%} of the wave cycles"]
     open(os.path.join(profiles, name + ".md"), "w").write("\n".join(lines) + "\n")
     mf = {}
     if os.path.isdir(mdir):
