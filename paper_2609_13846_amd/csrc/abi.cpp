@@ -465,23 +465,25 @@ dtp_status dtp_coordinate_ascent(int32_t N, int32_t G, int32_t I, int32_t L, con
     int32_t* nu_host = (int32_t*)(host.base + st_bytes + qu_bytes + qd_bytes);
     const int64_t* best = (const int64_t*)(host.base + best_off);
     DTP_HIP(hipMemcpyAsync(host.base, block.p, st_bytes + qu_bytes + qd_bytes, hipMemcpyDeviceToHost, s));
+    // The partition table is enumerated and queued while the stream encodes.  Every return
+    // below synchronises the stream before the guard releases the table's host copy.
+    ScoreWorkspace ws;
+    st = score_workspace_create(&ws, N, G, I, L, s);
+    struct WsGuard {
+      ScoreWorkspace* w;
+      hipStream_t s;
+      ~WsGuard() {
+        (void)hipStreamSynchronize(s);
+        score_workspace_destroy(w);
+      }
+    } guard{&ws, s};
+    if (st != DTP_OK) return st;
     DTP_HIP(hipStreamSynchronize(s));
     for (int m = 0; m < nmat; ++m) {
       st = m < N ? check_encode_stats(stats[m], "up affinity of layer", m)
                  : check_encode_stats(stats[m], "down affinity of layer", m - N);
       if (st != DTP_OK) return st;
     }
-
-    ScoreWorkspace ws;
-    st = score_workspace_create(&ws, N, G, I, L, s);
-    if (st != DTP_OK) {
-      score_workspace_destroy(&ws);
-      return st;
-    }
-    struct WsGuard {
-      ScoreWorkspace* w;
-      ~WsGuard() { score_workspace_destroy(w); }
-    } guard{&ws};
     const std::vector<uint8_t>& table = ws.host_table;
 
     // Contiguous start.

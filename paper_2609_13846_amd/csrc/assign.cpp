@@ -5,7 +5,8 @@
 // replicated slots per device.  The paper solves it approximately (dual ascent, a
 // capacity fix-up, pairwise swaps); this solver is exact.
 //
-// 1. Optimum.  With two devices, sorting by M[k][0] - M[k][1] is exact.  Otherwise neurons
+// 1. Optimum.  With two devices, a selection by M[k][0] - M[k][1] is exact and gives the
+//    canonical optimum of step 2 directly (canonical_two_devices).  Otherwise neurons
 //    are inserted one at a time, each along a best augmenting path of
 //    the current optimal partial assignment (the successive-shortest-path method of the
 //    assignment problem, one row at a time).  Because there are only L devices, a path is
@@ -22,6 +23,7 @@
 //    tight device that leaves a feasible completion, feasibility being Hall's condition
 //    over device subsets, evaluated by a subset-sum over tight-set masks.
 #include <algorithm>
+#include <functional>
 #include <queue>
 #include <utility>
 #include <vector>
@@ -183,13 +185,30 @@ void canonicalise(int I, int L, const int64_t* M, std::vector<int32_t>& nu) {
   }
 }
 
-// Two devices: an optimum puts the I/2 neurons with the largest M[k][0] - M[k][1] on
-// device 0 (exchanging any pair across the cut cannot gain).
-void optimal_two_devices(int I, const int64_t* M, std::vector<int32_t>& nu) {
-  std::vector<std::pair<int64_t, int32_t>> key(I);
-  for (int k = 0; k < I; ++k) key[k] = {M[2 * (size_t)k + 1] - M[2 * (size_t)k], k};
-  std::nth_element(key.begin(), key.begin() + I / 2, key.end());
-  for (int r = 0; r < I; ++r) nu[key[r].second] = r < I / 2 ? 0 : 1;
+// Two devices, optimum and canonical form in one pass.  An assignment is optimal exactly
+// when device 0 holds I/2 neurons of largest d_k = M[k][0] - M[k][1] (exchanging any pair
+// across the cut cannot gain), so the optima differ only in which neurons with d_k = t,
+// the I/2-th largest value, fill device 0's last places; the lexicographically smallest
+// gives those places to the lowest indices.
+void canonical_two_devices(int I, const int64_t* M, std::vector<int32_t>& nu) {
+  std::vector<int64_t> d(I);
+  for (int k = 0; k < I; ++k) d[k] = M[2 * (size_t)k] - M[2 * (size_t)k + 1];
+  std::vector<int64_t> sorted(d);
+  std::nth_element(sorted.begin(), sorted.begin() + (I / 2 - 1), sorted.end(), std::greater<int64_t>());
+  const int64_t t = sorted[I / 2 - 1];
+  int above = 0;
+  for (int k = 0; k < I; ++k) above += d[k] > t;
+  int ties_to_0 = I / 2 - above;  // >= 1: fewer than I/2 values exceed t, at least I/2 reach it
+  for (int k = 0; k < I; ++k) {
+    if (d[k] > t) {
+      nu[k] = 0;
+    } else if (d[k] == t && ties_to_0 > 0) {
+      nu[k] = 0;
+      --ties_to_0;
+    } else {
+      nu[k] = 1;
+    }
+  }
 }
 
 }  // namespace
@@ -199,11 +218,12 @@ void balanced_assign_exact(int I, int L, const int64_t* M, int32_t* nu_out, int6
   if (L == 1) {
     std::fill(nu.begin(), nu.end(), 0);
   } else {
-    if (L == 2)
-      optimal_two_devices(I, M, nu);
-    else
+    if (L == 2) {
+      canonical_two_devices(I, M, nu);
+    } else {
       optimal_by_insertion(I, L, M, nu);
-    canonicalise(I, L, M, nu);
+      canonicalise(I, L, M, nu);
+    }
   }
   int64_t v = 0;
   for (int k = 0; k < I; ++k) {
