@@ -4,7 +4,9 @@
 A step is one pass of the whole path over one layer's calibration batch: fold the
 weights, accumulate the first-order up affinity over all tokens, encode it, and run the
 coordinate ascent (exact neuron assignment on the host, partition scores on the GPU).
-The default workload is the Qwen3-0.6B-shaped layer: d=1024, I=3072, 16 query / 8 KV
+Steps run as a calibration over many layers runs them: step k's ascent on a second
+stream while step k+1's fold and affinity pass occupy the GPU (``serial_ms_per_step``
+gives the same steps one after another).  The default workload is the Qwen3-0.6B-shaped layer: d=1024, I=3072, 16 query / 8 KV
 heads of 128, 65,536 tokens, L=2 logical devices, bf16.  Inputs are synthetic and seeded
 (generated on the device before timing).
 
@@ -294,17 +296,43 @@ def main():
     log(f"workload {wl.name}: T={T} d={wl.d_model} I={I} H={wl.n_q_heads} G={G} dh={wl.head_dim} L={L}")
     layer, w = make_layer(dtp, synth, wl, 0, device)
     x, attn = synth.device_tokens(wl, 0, w, T, 0, device)
-    A = torch.zeros(G, I, dtype=torch.float32, device=device)
+    # Two affinity buffers: a step's ascent reads one while the next step's affinity fills
+    # the other.
+    A_buf = [torch.zeros(G, I, dtype=torch.float32, device=device) for _ in range(2)]
+    A = A_buf[0]
+    main_stream = torch.cuda.current_stream()
+    ascent_stream = torch.cuda.Stream()  # default priority
     torch.cuda.synchronize()
 
-    def step():
+    def gpu_part(Ak):
         dtp.dtp_layer_set_weights(layer, w["w_o"], w["gamma"], w["w_gate"], w["w_up"], w["w_down"])
-        A.zero_()
-        dtp.dtp_affinity_accumulate(layer, x, attn, T, A)
+        Ak.zero_()
+        dtp.dtp_affinity_accumulate(layer, x, attn, T, Ak)
+
+    def step():
+        gpu_part(A)
         return dtp.dtp_coordinate_ascent(1, G, I, L, A)   # synchronises the stream
+
+    def pipelined_steps(K):
+        """K steps, each the fold, the affinity pass and the ascent of one layer, as a
+        calibration over many layers runs them: step k's ascent (host neuron steps, small
+        kernels) on a second stream while step k+1's fold and affinity occupy the GPU."""
+        done = [torch.cuda.Event() for _ in range(2)]
+        gpu_part(A_buf[0])
+        done[0].record(main_stream)
+        r = None
+        for k in range(K):
+            if k + 1 < K:
+                gpu_part(A_buf[(k + 1) % 2])
+                done[(k + 1) % 2].record(main_stream)
+            ascent_stream.wait_event(done[k % 2])
+            r = dtp.dtp_coordinate_ascent(1, G, I, L, A_buf[k % 2], stream=ascent_stream)
+            main_stream.wait_stream(ascent_stream)  # the buffer's next fill follows its ascent
+        return r
 
     for _ in range(args.warmup):
         res = step()
+    pipelined_steps(2)
     # phase breakdown (untimed pass with synchronisation between phases)
     torch.cuda.synchronize()
     b0 = time.perf_counter()
@@ -317,13 +345,19 @@ def main():
     b2 = time.perf_counter()
     dtp.dtp_coordinate_ascent(1, G, I, L, A)
     b3 = time.perf_counter()
+    # the same steps one after another, each ascent waiting for its own affinity pass
+    torch.cuda.synchronize()
+    s0 = time.perf_counter()
+    for _ in range(args.steps):
+        step()
+    torch.cuda.synchronize()
+    serial_ms = (time.perf_counter() - s0) * 1e3 / args.steps
 
     log(f"timing {args.steps} steps")
     dtp.dtp_layer_profile(layer, 1)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
-    for _ in range(args.steps):
-        res = step()
+    res = pipelined_steps(args.steps)
     torch.cuda.synchronize()
     t1 = time.perf_counter()
     kern_ms, launches = dtp.dtp_layer_profile_read(layer)
@@ -374,6 +408,9 @@ def main():
                      "tokens_per_launch": T / max(launches_per_step, 1),
                      "flops_per_launch": f_launch},
         "step_tflops": flops_per_token(wl) * T / (ms_per_step * 1e-3) / 1e12,
+        "pipelining": "step k's ascent runs on a second stream beside step k+1's fold and "
+                      "affinity; every step does all its work",
+        "serial_ms_per_step": serial_ms,
         "breakdown_ms": {"fold": (b1 - b0) * 1e3, "affinity": (b2 - b1) * 1e3,
                          "layout": (b3 - b2) * 1e3},
         "layout": {"J": res["J"], "sweeps": res["sweeps"], "neuron_step": neuron_steps,
