@@ -208,3 +208,49 @@ def test_concurrent_ascents_from_several_threads_match_serial():
         np.testing.assert_array_equal(res["nu"], ref["nu"])
         assert res["J_fixed"] == ref["J_fixed"] and res["sweeps"] == ref["sweeps"]
     assert all(s == dtp.DTP_ERR_DEGENERATE for s in errors.values()) and len(errors) == 12
+
+
+def test_ascent_beside_the_next_affinity_pass_matches_serial():
+    """Steps as a calibration over many layers runs them (and as bench.py times them): step
+    k's ascent on a second stream, after an event marking its affinity pass done, while
+    step k+1's fold and affinity pass fill the other of two buffers on the first stream.
+    Each step's layout, J and sweep count equal the same step run alone."""
+    announce("ascent beside the next affinity pass, 4 steps")
+    wl = synth.WORKLOADS["qwen3-0.6b-layer"]
+    G, I, L, T = wl.n_kv_groups, wl.n_neurons, 2, 8192
+    dev = torch.device("cuda", 0)
+    w = synth.device_weights(wl, 0, dev)
+    toks = [synth.device_tokens(wl, 0, w, T, c, dev) for c in range(4)]
+    layer = hp.layer_for(wl)
+    try:
+        def gpu_part(c, A):
+            dtp.dtp_layer_set_weights(layer, w["w_o"], w["gamma"], w["w_gate"], w["w_up"], w["w_down"])
+            A.zero_()
+            dtp.dtp_affinity_accumulate(layer, toks[c][0], toks[c][1], T, A)
+
+        A = torch.zeros(G, I, device=dev)
+        serial = []
+        for c in range(4):
+            gpu_part(c, A)
+            serial.append(dtp.dtp_coordinate_ascent(1, G, I, L, A))
+        bufs = [torch.zeros(G, I, device=dev) for _ in range(2)]
+        main, side = torch.cuda.current_stream(), torch.cuda.Stream()
+        done = [torch.cuda.Event() for _ in range(2)]
+        piped = []
+        gpu_part(0, bufs[0])
+        done[0].record(main)
+        for k in range(4):
+            if k + 1 < 4:
+                gpu_part(k + 1, bufs[(k + 1) % 2])
+                done[(k + 1) % 2].record(main)
+            side.wait_event(done[k % 2])
+            piped.append(dtp.dtp_coordinate_ascent(1, G, I, L, bufs[k % 2], stream=side))
+            main.wait_stream(side)
+        torch.cuda.synchronize()
+    finally:
+        dtp.dtp_layer_destroy(layer)
+    assert len({r["J_fixed"] for r in serial}) > 1  # the steps differ
+    for r, ref in zip(piped, serial):
+        np.testing.assert_array_equal(r["h"], ref["h"])
+        np.testing.assert_array_equal(r["nu"], ref["nu"])
+        assert r["J_fixed"] == ref["J_fixed"] and r["sweeps"] == ref["sweeps"]
