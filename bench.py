@@ -33,7 +33,7 @@ sys.path.insert(0, ROOT)
 PEAK_BF16_TFLOPS = 2516.6   # MI355X dense bf16 MFMA
 METRIC = "affinity calibration tokens/s per layer + % bf16 MFMA peak; full-model layout time"
 KERNEL_SRC = os.path.join(ROOT, "paper_2609_13846_amd", "csrc", "affinity.hip")
-TRAFFIC_FILE = os.path.join(ROOT, "profiles", "affinity_traffic.json")
+PROFILES = os.path.join(ROOT, "profiles")
 
 
 def log(msg):
@@ -53,7 +53,7 @@ def traffic_record(wl):
     """The committed PMC summary of the affinity kernel (HBM bytes, MFMA busy fraction and
     clock per launch), if it was taken on this kernel source and workload; else {}."""
     try:
-        rec = json.load(open(TRAFFIC_FILE))
+        rec = json.load(open(os.path.join(PROFILES, f"affinity_traffic_{wl.name}.json")))
     except (OSError, ValueError):
         return {}
     if rec.get("kernel_sha") != kernel_hash() or rec.get("workload") != wl.name:

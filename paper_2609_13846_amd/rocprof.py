@@ -1,9 +1,11 @@
 """Collect and summarise rocprofv3 runs of bench.py (kernel timing and HBM traffic).
 
-    python -m paper_2609_13846_amd.rocprof collect --out <dir>
-    python -m paper_2609_13846_amd.rocprof summarize --dir <dir> --profiles profiles
+    python -m paper_2609_13846_amd.rocprof collect --out <dir> [--workload NAME]
+    python -m paper_2609_13846_amd.rocprof summarize --dir <dir> --profiles profiles [--workload NAME]
 
-``collect`` runs six rocprofv3 passes of ``bench.py``, each in its own process with its
+(NAME: a workload of ``synth.WORKLOADS``, the Qwen3-0.6B-shaped layer by default.)
+
+``collect`` runs seven rocprofv3 passes of ``bench.py``, each in its own process with its
 own time limit, writing CSV output (no database files):
 
 * ``trace``: ``--kernel-trace --stats`` of a timed bench run;
@@ -54,9 +56,19 @@ def kernel_sha() -> str:
     return hashlib.sha256(open(KERNEL_SRC, "rb").read()).hexdigest()[:16]
 
 
-def _passes(out: str, steps: int):
+DEFAULT_WORKLOAD = "qwen3-0.6b-layer"
+
+
+def traffic_file(profiles: str, workload: str) -> str:
+    """The JSON record of one workload's affinity-kernel counters."""
+    return os.path.join(profiles, f"affinity_traffic_{workload}.json")
+
+
+def _passes(out: str, steps: int, workload: str = DEFAULT_WORKLOAD):
     bench = [sys.executable, os.path.join(ROOT, "bench.py")]
     quiet = ["--no-cpu-baseline", "--no-library-gemm", "--no-full-model"]
+    if workload != DEFAULT_WORKLOAD:
+        quiet += ["--workload", workload]
     timed = bench + ["--steps", str(steps), "--warmup", "2", *quiet]
     short = bench + ["--steps", "2", "--warmup", "1", *quiet]
     copy = bench + ["--copy-calibration", str(COPY_MIB)]
@@ -71,11 +83,11 @@ def _passes(out: str, steps: int):
     ]
 
 
-def collect(out: str, steps: int) -> int:
+def collect(out: str, steps: int, workload: str = DEFAULT_WORKLOAD) -> int:
     out = os.path.abspath(out)
     os.makedirs(out, exist_ok=True)
     env = dict(os.environ, TMPDIR="/tmp")
-    for name, opts, cmd, limit in _passes(out, steps):
+    for name, opts, cmd, limit in _passes(out, steps, workload):
         full = ["timeout", "-s", "KILL", str(limit), "rocprofv3", *opts, "--output-format", "csv",
                 "-d", os.path.join(out, name), "-o", "run", "--", *cmd]
         print(f"[rocprof] pass {name}: {' '.join(full)}", flush=True)
@@ -85,7 +97,7 @@ def collect(out: str, steps: int) -> int:
             print(f"[rocprof] pass {name} failed with {rc}", flush=True)
             return rc
     with open(os.path.join(out, "commands.txt"), "w") as f:
-        for name, opts, cmd, limit in _passes(out, steps):
+        for name, opts, cmd, limit in _passes(out, steps, workload):
             shown = ["python3" if c == sys.executable else
                      (os.path.relpath(c, ROOT) if c.startswith(ROOT) else c) for c in cmd]
             f.write(f"{name}: rocprofv3 {' '.join(opts)} --output-format csv -d <dir>/{name} -o run -- "
@@ -142,8 +154,9 @@ def summarize(d: str, profiles: str, workload: str, bench_cmd: str) -> None:
     lines = [f"# rocprofv3 summary: affinity kernel, {workload} workload", "",
              "Commands (run from the repository root on one MI355X):", "", "```"]
     lines += [l.rstrip() for l in open(os.path.join(d, "commands.txt"))]
+    wl_opt = f" --workload {workload}" if workload != DEFAULT_WORKLOAD else ""
     lines += ["```", "", f"Summarised with `python -m paper_2609_13846_amd.rocprof summarize --dir <dir> "
-              f"--profiles profiles` (kernel source sha256 prefix `{kernel_sha()}`).", "",
+              f"--profiles profiles{wl_opt}` (kernel source sha256 prefix `{kernel_sha()}`).", "",
               "## Kernel trace (--kernel-trace --stats), top kernels", "",
               "| kernel | calls | avg (us) | total (ms) | share |", "|---|---:|---:|---:|---:|"]
     for r in stats[:12]:
@@ -215,8 +228,8 @@ def summarize(d: str, profiles: str, workload: str, bench_cmd: str) -> None:
            "fetch_bytes_per_launch": fetch_b, "write_bytes_per_launch": write_b,
            "bytes_per_launch": fetch_b + write_b, "fetch_scale": f_scale, "write_scale": w_scale,
            "avg_launch_us": float(aff[0]["AverageNs"]) / 1e3 if aff else None, **mf}
-    json.dump(rec, open(os.path.join(profiles, "affinity_traffic.json"), "w"), indent=1)
-    print(f"wrote {os.path.join(profiles, name + '.md')} and affinity_traffic.json")
+    json.dump(rec, open(traffic_file(profiles, workload), "w"), indent=1)
+    print(f"wrote {os.path.join(profiles, name + '.md')} and {os.path.basename(traffic_file(profiles, workload))}")
 
 
 def main():
@@ -225,13 +238,14 @@ def main():
     c = sub.add_parser("collect")
     c.add_argument("--out", required=True)
     c.add_argument("--steps", type=int, default=5)
+    c.add_argument("--workload", default=DEFAULT_WORKLOAD)
     s = sub.add_parser("summarize")
     s.add_argument("--dir", required=True)
     s.add_argument("--profiles", default=os.path.join(ROOT, "profiles"))
-    s.add_argument("--workload", default="qwen3-0.6b-layer")
+    s.add_argument("--workload", default=DEFAULT_WORKLOAD)
     args = ap.parse_args()
     if args.cmd == "collect":
-        sys.exit(collect(args.out, args.steps))
+        sys.exit(collect(args.out, args.steps, args.workload))
     summarize(args.dir, args.profiles, args.workload, "")
 
 
