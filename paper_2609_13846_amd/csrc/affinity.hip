@@ -1001,6 +1001,43 @@ bool affinity_lds_fits(size_t dynamic, size_t margin = 0) {
   return static_lds + dynamic + margin <= kLdsPerCu;
 }
 
+// Compute units of the current device (cached per device).
+int device_cus() {
+  static int cus[64] = {0};
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 256;
+  if (cus[dev] == 0) {
+    int n = 0;
+    cus[dev] = hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess && n > 0
+                   ? n : 256;
+  }
+  return cus[dev];
+}
+
+// Token splits of a launch.  A CU runs one block of the fused kernel at a time (its eight
+// waves fill the register file), so blocks run in rounds of one per CU and the last
+// round decides the launch's length: 896 blocks take four rounds of 256 CUs where 1,792
+// of half the work each take seven, 12.5% sooner.  From the smallest split count that
+// reaches kTargetBlocks, up to four times it, take the first count whose blocks fill
+// their rounds best.
+int choose_splits(int groups, int mtiles) {
+  const int cap = std::min(mtiles, kMaxSplits);
+  const int lo = std::max(1, std::min((kTargetBlocks + groups - 1) / groups, cap));
+  const int64_t cus = device_cus();
+  int best = lo;
+  int64_t best_num = 0, best_den = 1;  // fill = blocks / (rounds * cus)
+  for (int s = lo; s <= std::min(4 * lo, cap); ++s) {
+    const int64_t blocks = (int64_t)groups * s;
+    const int64_t den = (blocks + cus - 1) / cus * cus;
+    if (blocks * best_den > best_num * den) {
+      best = s;
+      best_num = blocks;
+      best_den = den;
+    }
+  }
+  return best;
+}
+
 // Launches the fused kernel on one slice; returns the number of token splits used, or 0
 // if a block does not fit the LDS.
 template <int KC, int WM, int WN, int RB, int NB, bool PACK, int SG, bool ADD, int RING>
@@ -1009,7 +1046,7 @@ int launch_affinity(AffinityArgs p, hipStream_t s) {
   constexpr int kNeurons = 32 * NB * WN;
   const int groups = p.n_tiles * kBN / kNeurons;
   const int mtiles = (p.T + kRows - 1) / kRows;
-  p.splits = std::max(1, std::min((kTargetBlocks + groups - 1) / groups, std::min(mtiles, kMaxSplits)));
+  p.splits = choose_splits(groups, mtiles);
   const size_t shm = affinity_dynamic_lds<WM, WN, NB>(p.G);
   if (!affinity_lds_fits<KC, WM, WN, RB, NB, PACK, SG, ADD, RING>(shm)) return 0;
   if (shm > 65536)  // beyond the default dynamic LDS limit (G close to 32)
