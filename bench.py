@@ -332,6 +332,9 @@ def main():
 
     for _ in range(args.warmup):
         res = step()
+    # The second stream's first ascent sets up its stream-ordered memory; done here, with
+    # the GPU otherwise idle, it does not stall an affinity launch running beside it.
+    dtp.dtp_coordinate_ascent(1, G, I, L, A, stream=ascent_stream)
     pipelined_steps(2)
     # phase breakdown (untimed pass with synchronisation between phases)
     torch.cuda.synchronize()
