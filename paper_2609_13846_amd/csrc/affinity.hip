@@ -1015,24 +1015,25 @@ int device_cus() {
 }
 
 // Token splits of a launch.  A CU runs one block of the fused kernel at a time (its eight
-// waves fill the register file), so blocks run in rounds of one per CU and the last
-// round decides the launch's length: 896 blocks take four rounds of 256 CUs where 1,792
-// of half the work each take seven, 12.5% sooner.  From the smallest split count that
-// reaches kTargetBlocks, up to four times it, take the first count whose blocks fill
-// their rounds best.
+// waves fill the register file), so blocks run in rounds of one per CU, and a block of a
+// launch with S splits takes up to ceil(mtiles / S) token tiles: the launch lasts about
+// ceil(groups * S / CUs) * ceil(mtiles / S) tile times.  From the smallest split count
+// that reaches kTargetBlocks, up to four times it, take the first count that minimises
+// that product.  (896 blocks of 32 tiles take four rounds of 256 CUs where 1,792 blocks
+// of 16 take seven, 12.5% sooner; 768 blocks of up to 6 tiles take 18 units where 1,024
+// of 4 take 16.)
 int choose_splits(int groups, int mtiles) {
   const int cap = std::min(mtiles, kMaxSplits);
   const int lo = std::max(1, std::min((kTargetBlocks + groups - 1) / groups, cap));
   const int64_t cus = device_cus();
   int best = lo;
-  int64_t best_num = 0, best_den = 1;  // fill = blocks / (rounds * cus)
+  int64_t best_cost = -1;
   for (int s = lo; s <= std::min(4 * lo, cap); ++s) {
-    const int64_t blocks = (int64_t)groups * s;
-    const int64_t den = (blocks + cus - 1) / cus * cus;
-    if (blocks * best_den > best_num * den) {
+    const int64_t rounds = ((int64_t)groups * s + cus - 1) / cus;
+    const int64_t cost = rounds * ((mtiles + s - 1) / s);
+    if (best_cost < 0 || cost < best_cost) {
       best = s;
-      best_num = blocks;
-      best_den = den;
+      best_cost = cost;
     }
   }
   return best;
