@@ -6,9 +6,9 @@ weights, accumulate the first-order up affinity over all tokens, encode it, and 
 coordinate ascent (exact neuron assignment on the host, partition scores on the GPU).
 Steps run as a calibration over many layers runs them: step k's ascent on a second
 stream while step k+1's fold and affinity pass occupy the GPU (``serial_ms_per_step``
-gives the same steps one after another).  The default workload is the Qwen3-0.6B-shaped layer: d=1024, I=3072, 16 query / 8 KV
-heads of 128, 65,536 tokens, L=2 logical devices, bf16.  Inputs are synthetic and seeded
-(generated on the device before timing).
+gives the same steps one after another).  The default workload is the Qwen3-0.6B-shaped
+layer: d=1024, I=3072, 16 query / 8 KV heads of 128, 65,536 tokens, L=2 logical devices,
+bf16.  Inputs are synthetic and seeded (generated on the device before timing).
 
 The JSON line reports calibration tokens/s per layer (value), the MFMA roofline of the
 dominant kernel timed with HIP events on its launch stream, and the fp64 oracle timed on
