@@ -40,6 +40,7 @@ def oracle(wl, w, x, a, neurons=None):
     ("qwen3-0.6b-layer", 300, {}),
     ("danube3-500m", 257, {}),
     ("qwen3-0.6b-layer", 200, dict(n_neurons=1000)),               # ragged neuron tile
+    ("qwen3-0.6b-layer", 150, dict(n_neurons=1003)),               # I % 8 != 0: scalar norm pass
     ("qwen3-0.6b-layer", 130, dict(n_q_heads=2, n_kv_groups=1)),    # one group
     ("qwen3-0.6b-layer", 129, dict(n_q_heads=8, n_kv_groups=8, head_dim=48)),  # H = G, dh % 32 = 16
     ("qwen3-0.6b-layer", 100, dict(n_q_heads=32, n_kv_groups=32, head_dim=64)),  # G at its limit
@@ -62,6 +63,35 @@ def test_affinity_matches_oracle(name, T, shape):
     announce(f"affinity {name} T={T} {shape}")
     A = hp.gpu_affinity(wl, w, x, a)
     hp.assert_affinity_close(A, oracle(wl, w, x, a))
+
+
+def test_unaligned_down_weights_give_the_same_affinity():
+    """W_down at an address 2 bytes past a 16-byte boundary takes the norms' scalar pass
+    instead of its 16-byte loads; each column is summed in the same order either way, so
+    the affinity is bit-identical."""
+    import torch
+    wl, w, x, a = case("qwen3-0.6b-layer", 300)
+    announce("affinity with W_down 2 bytes off a 16-byte boundary")
+    dw = [hp.torch_dev(v) for v in (w.w_o, w.gamma, w.w_gate, w.w_up, w.w_down)]
+    wd = dw[4].reshape(-1)
+    shifted = torch.empty(wd.numel() + 8, dtype=wd.dtype, device="cuda")
+    shifted[1:1 + wd.numel()].copy_(wd)
+    wd_off = shifted[1:1 + wd.numel()]
+    assert wd_off.data_ptr() % 16 == 2
+    dx, da = hp.torch_dev(x), hp.torch_dev(a)
+    out = []
+    for w_down in (dw[4], wd_off):
+        layer = hp.layer_for(wl)
+        try:
+            dtp.dtp_layer_set_weights(layer, dw[0], dw[1], dw[2], dw[3], w_down)
+            A = torch.zeros(wl.n_kv_groups, wl.n_neurons, dtype=torch.float32, device="cuda")
+            dtp.dtp_affinity_accumulate(layer, dx, da, x.shape[0], A)
+            torch.cuda.synchronize()
+            out.append(A.cpu().numpy())
+        finally:
+            dtp.dtp_layer_destroy(layer)
+    np.testing.assert_array_equal(out[0], out[1])
+    hp.assert_affinity_close(out[1], oracle(wl, w, x, a))
 
 
 def test_affinity_8b_class_sampled_neurons():
