@@ -30,6 +30,7 @@
 // per slice so that every fragment load is contiguous; the fused kernel is one
 // contraction over d + H*dh with epilogues at the operating-point and head boundaries.
 // The fp32 path (dtype DTP_F32) runs the same decomposition with plain FMA kernels.
+#include <atomic>
 #include <cmath>
 #include <vector>
 
@@ -1001,17 +1002,19 @@ bool affinity_lds_fits(size_t dynamic, size_t margin = 0) {
   return static_lds + dynamic + margin <= kLdsPerCu;
 }
 
-// Compute units of the current device (cached per device).
+// Compute units of the current device, cached per device (atomics: calls on different
+// layers may run on several host threads at once).
 int device_cus() {
-  static int cus[64] = {0};
+  static std::atomic<int> cus[64];
   int dev = 0;
   if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 256;
-  if (cus[dev] == 0) {
-    int n = 0;
-    cus[dev] = hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess && n > 0
-                   ? n : 256;
+  int n = cus[dev].load(std::memory_order_relaxed);
+  if (n == 0) {
+    if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0)
+      n = 256;
+    cus[dev].store(n, std::memory_order_relaxed);
   }
-  return cus[dev];
+  return n;
 }
 
 // Token splits of a launch.  A CU runs one block of the fused kernel at a time (its eight
