@@ -130,16 +130,18 @@ dtp_status dtp_affinity_accumulate_down(dtp_layer layer, const void* x, const vo
  *   B dev [G, I] float                          written
  * bf16: MFMA over d with gamma' * w^d_k rounded to bf16, fp32 sums of squares; requires
  * d and I multiples of 8.  f32: plain FMAs (small shapes).  Scratch of G*I*ceil((H/G+2)*dh
- * /128) floats is taken from the stream-ordered allocator and returned before exit. */
+ * /128) floats, and for bf16 a gamma'-scaled transposed copy of W_down (I*d bf16), is taken
+ * from the stream-ordered allocator and returned before exit. */
 dtp_status dtp_down_weights(int32_t d_model, int32_t n_neurons, int32_t n_q_heads,
                             int32_t n_kv_groups, int32_t head_dim, dtp_dtype dtype,
                             const void* w_q, const void* w_k, const void* w_v,
                             const void* gamma_next, const void* w_down, float* B, void* stream);
 
 /* dtp_down_weights for callers that cannot allocate device memory (code under HIP graph
- * capture, serving loops and harnesses that forbid hipMalloc): the same kernels and the same
- * B bit for bit, with the per-chunk partial sums in a fixed 4 MiB device array instead of
- * stream-ordered scratch.  The call makes no allocation of any kind; the array is held by
+ * capture, serving loops and harnesses that forbid hipMalloc): the same B bit for bit, with
+ * the per-chunk partial sums in a fixed 4 MiB device array instead of stream-ordered scratch,
+ * and W_down scaled and transposed stage by stage inside the weight kernel instead of once
+ * into a copy.  The call makes no allocation of any kind; the array is held by
  * each device the library runs on until the process ends (its address is looked up once per
  * device, on the first call there).  Limit: G * I * ceil((H/G + 2) * dh / 128) <= 2^20
  * partial sums (the 8B-class shape needs 688,128), else DTP_ERR_UNSUPPORTED before any

@@ -11,6 +11,7 @@
 // then its k rows and its v rows, from the q_proj / k_proj / v_proj weight layouts.
 //
 // Kernels:
+//   scale_transpose_down_kernel  gamma' * W_down transposed to [I][d] bf16, once per call
 //   down_weight_bf16_kernel  one block per (128 neurons, 128 rows of W^{qkv}_g, group):
 //                            MFMA over d, then per-column sums of squares of the 128 rows
 //   down_weight_f32_kernel   the same with plain FMAs, one thread per (group, neuron)
@@ -40,14 +41,42 @@ __device__ inline const T* qkv_row(const T* w_q, const T* w_k, const T* w_v, int
   return w_v + ((int64_t)g * dh + rho - dh) * d;
 }
 
+// tw[k][j] = bf16(w_down[j][k] * gamma'[j]): W_down scaled and transposed once per call, so
+// that the weight kernel reads each neuron's column contiguous along the contraction
+// instead of scaling and transposing it again for every group and row chunk.  64 x 64
+// tiles through LDS, reads along k and writes along j.
+__global__ void __launch_bounds__(256)
+scale_transpose_down_kernel(const uint16_t* __restrict__ w_down, const uint16_t* __restrict__ gamma,
+                            int d, int I, uint16_t* __restrict__ tw) {
+  __shared__ uint16_t tile[64][64 + 2];
+  const int k0 = blockIdx.x * 64, j0 = blockIdx.y * 64;
+  for (int idx = threadIdx.x; idx < 64 * 64; idx += 256) {
+    const int r = idx / 64, c = idx % 64;
+    const int j = j0 + r, k = k0 + c;
+    tile[r][c] = j < d && k < I
+                     ? f32_to_bf16(bf16_to_f32(w_down[(int64_t)j * I + k]) * bf16_to_f32(gamma[j]))
+                     : (uint16_t)0;
+  }
+  __syncthreads();
+  for (int idx = threadIdx.x; idx < 64 * 64; idx += 256) {
+    const int r = idx / 64, c = idx % 64;
+    const int k = k0 + r, j = j0 + c;
+    if (k < I && j < d) tw[(int64_t)k * d + j] = tile[c][r];
+  }
+}
+
 // partial[g][chunk][k] = sum over the chunk's rows rho of (W^{qkv}_g[rho] . (gamma' * w^d_k))^2.
+// TW: the B operand comes from scale_transpose_down_kernel's tw; otherwise each stage
+// scales and transposes its slice of W_down itself (the allocation-free path, which has no
+// room for tw).  Both fill the LDS tile with the same values, so B is the same to the bit.
+template <bool TW>
 __global__ void __launch_bounds__(kTileThreads)
 down_weight_bf16_kernel(const uint16_t* __restrict__ w_q, const uint16_t* __restrict__ w_k,
                         const uint16_t* __restrict__ w_v, const uint16_t* __restrict__ gamma,
-                        const uint16_t* __restrict__ w_down, int d, int I, int hpg, int dh,
-                        float* __restrict__ partial) {
-  __shared__ __attribute__((aligned(16))) uint16_t As[kDRows * kDRow];
-  __shared__ __attribute__((aligned(16))) uint16_t Bs[kDCols * kDRow];
+                        const uint16_t* __restrict__ w_down, const uint16_t* __restrict__ tw,
+                        int d, int I, int hpg, int dh, float* __restrict__ partial) {
+  __shared__ __attribute__((aligned(16))) uint16_t As[2][kDRows * kDRow];
+  __shared__ __attribute__((aligned(16))) uint16_t Bs[2][kDCols * kDRow];
   __shared__ float red[4][kDCols];
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int k0 = blockIdx.x * kDCols, chunk = blockIdx.y, g = blockIdx.z;
@@ -56,34 +85,68 @@ down_weight_bf16_kernel(const uint16_t* __restrict__ w_q, const uint16_t* __rest
   f32x16 acc[4];
 #pragma unroll
   for (int b = 0; b < 4; ++b) acc[b] = f32x16{};
-  for (int kc = 0; kc < d; kc += kDKC) {
-    // A: 128 rows x 32 columns of W^{qkv}_g, 16 bytes per thread and pass (2 passes).
+  // A stage's operands in registers: A, 128 rows x 32 columns of W^{qkv}_g, and B, 128
+  // neurons x 32 columns of gamma' * W_down, 16 bytes per thread and pass (2 passes each).
+  // Stage kc+32 is fetched into registers during stage kc's MFMAs and stored into the
+  // other LDS buffer after them.
+  u32x4 av[2], bv[2];
+  float bg[2];
+  auto fetch = [&](int kc) __attribute__((always_inline)) {
 #pragma unroll
     for (int pass = 0; pass < 2; ++pass) {
       const int row = threadIdx.x / 4 + 64 * pass, seg = threadIdx.x % 4;
       const int rho = chunk * kDRows + row, j = kc + 8 * seg;
-      u32x4 v = {0u, 0u, 0u, 0u};
+      av[pass] = u32x4{0u, 0u, 0u, 0u};
       if (rho < R && j < d)
-        v = *reinterpret_cast<const u32x4*>(qkv_row(w_q, w_k, w_v, g, rho, hpg, dh, d) + j);
-      *reinterpret_cast<u32x4*>(As + row * kDRow + 8 * seg) = v;
+        av[pass] = *reinterpret_cast<const u32x4*>(qkv_row(w_q, w_k, w_v, g, rho, hpg, dh, d) + j);
     }
-    // B: 32 rows j of W_down x 128 neurons, times gamma'[j], stored transposed [k][j].
 #pragma unroll
     for (int pass = 0; pass < 2; ++pass) {
-      const int idx = threadIdx.x + kTileThreads * pass;
-      const int jj = idx / 16, kseg = idx % 16;
-      const int j = kc + jj, k = k0 + 8 * kseg;
-      u32x4 v = {0u, 0u, 0u, 0u};  // I % 8 == 0: the 8 neurons are all valid or all past I
-      if (j < d && k < I) v = *reinterpret_cast<const u32x4*>(w_down + (int64_t)j * I + k);
-      const float gj = j < d ? bf16_to_f32(gamma[j]) : 0.0f;
-#pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        const uint16_t w = (uint16_t)(v[e / 2] >> (16 * (e % 2)));
-        Bs[(8 * kseg + e) * kDRow + jj] = f32_to_bf16(bf16_to_f32(w) * gj);
+      bv[pass] = u32x4{0u, 0u, 0u, 0u};
+      if constexpr (TW) {
+        const int row = threadIdx.x / 4 + 64 * pass, seg = threadIdx.x % 4;
+        const int k = k0 + row, j = kc + 8 * seg;
+        if (k < I && j < d) bv[pass] = *reinterpret_cast<const u32x4*>(tw + (int64_t)k * d + j);
+      } else {
+        const int idx = threadIdx.x + kTileThreads * pass;
+        const int jj = idx / 16, kseg = idx % 16;
+        const int j = kc + jj, k = k0 + 8 * kseg;
+        // I % 8 == 0: the 8 neurons are all valid or all past I
+        if (j < d && k < I) bv[pass] = *reinterpret_cast<const u32x4*>(w_down + (int64_t)j * I + k);
+        bg[pass] = j < d ? bf16_to_f32(gamma[j]) : 0.0f;
       }
     }
-    __syncthreads();
-    mfma_stage<kDKC>(As, Bs, acc, wave, lane);
+  };
+  auto store = [&](int buf) __attribute__((always_inline)) {
+#pragma unroll
+    for (int pass = 0; pass < 2; ++pass) {
+      const int row = threadIdx.x / 4 + 64 * pass, seg = threadIdx.x % 4;
+      *reinterpret_cast<u32x4*>(As[buf] + row * kDRow + 8 * seg) = av[pass];
+    }
+#pragma unroll
+    for (int pass = 0; pass < 2; ++pass) {
+      if constexpr (TW) {
+        const int row = threadIdx.x / 4 + 64 * pass, seg = threadIdx.x % 4;
+        *reinterpret_cast<u32x4*>(Bs[buf] + row * kDRow + 8 * seg) = bv[pass];
+      } else {  // scaled by gamma'[j] and stored transposed, [k][j]
+        const int idx = threadIdx.x + kTileThreads * pass;
+        const int jj = idx / 16, kseg = idx % 16;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          const uint16_t w = (uint16_t)(bv[pass][e / 2] >> (16 * (e % 2)));
+          Bs[buf][(8 * kseg + e) * kDRow + jj] = f32_to_bf16(bf16_to_f32(w) * bg[pass]);
+        }
+      }
+    }
+  };
+  fetch(0);
+  store(0);
+  __syncthreads();
+  for (int kc = 0, buf = 0; kc < d; kc += kDKC, buf ^= 1) {
+    const bool more = kc + kDKC < d;
+    if (more) fetch(kc + kDKC);
+    mfma_stage<kDKC>(As[buf], Bs[buf], acc, wave, lane);
+    if (more) store(buf ^ 1);
     __syncthreads();
   }
   // Sum of squares over the wave's 32 rows, per column; rows past R are zero.
@@ -228,26 +291,47 @@ dtp_status down_weights(int32_t d_model, int32_t n_neurons, int32_t n_q_heads, i
   DTP_CHECK(n_neurons % 8 == 0, DTP_ERR_INVALID_ARG, "n_neurons=%d is not a multiple of 8",
             n_neurons);
   float* partial = nullptr;
+  uint16_t* tw = nullptr;
   if (use_static) {
     dtp_status st = noalloc_scratch(&partial);
     if (st != DTP_OK) return st;
   } else {
     DTP_HIP(hipMallocAsync((void**)&partial, sizeof(float) * (size_t)GI * n_chunks, s));
+    const hipError_t ea = hipMallocAsync((void**)&tw, sizeof(uint16_t) * (size_t)n_neurons * d_model, s);
+    if (ea != hipSuccess) {
+      (void)hipFreeAsync(partial, s);
+      DTP_HIP(ea);
+    }
   }
   dim3 grid((n_neurons + kDCols - 1) / kDCols, n_chunks, n_kv_groups);
-  down_weight_bf16_kernel<<<grid, kTileThreads, 0, s>>>(
-      (const uint16_t*)w_q, (const uint16_t*)w_k, (const uint16_t*)w_v,
-      (const uint16_t*)gamma_next, (const uint16_t*)w_down, d_model, n_neurons, hpg, head_dim,
-      partial);
-  hipError_t e = hipGetLastError();
+  hipError_t e = hipSuccess;
+  if (tw) {
+    const dim3 tg((n_neurons + 63) / 64, (d_model + 63) / 64);
+    scale_transpose_down_kernel<<<tg, 256, 0, s>>>((const uint16_t*)w_down,
+                                                   (const uint16_t*)gamma_next, d_model, n_neurons, tw);
+    e = hipGetLastError();
+    if (e == hipSuccess)
+      down_weight_bf16_kernel<true><<<grid, kTileThreads, 0, s>>>(
+          (const uint16_t*)w_q, (const uint16_t*)w_k, (const uint16_t*)w_v,
+          (const uint16_t*)gamma_next, (const uint16_t*)w_down, tw, d_model, n_neurons, hpg,
+          head_dim, partial);
+  } else {
+    down_weight_bf16_kernel<false><<<grid, kTileThreads, 0, s>>>(
+        (const uint16_t*)w_q, (const uint16_t*)w_k, (const uint16_t*)w_v,
+        (const uint16_t*)gamma_next, (const uint16_t*)w_down, nullptr, d_model, n_neurons, hpg,
+        head_dim, partial);
+  }
+  if (e == hipSuccess) e = hipGetLastError();
   if (e == hipSuccess) {
     down_rows_reduce_kernel<<<blocks_for(GI, 256), 256, 0, s>>>(partial, n_kv_groups, n_chunks,
                                                                 n_neurons, B);
     e = hipGetLastError();
   }
   const hipError_t ef = use_static ? hipSuccess : hipFreeAsync(partial, s);
+  const hipError_t et = tw ? hipFreeAsync(tw, s) : hipSuccess;
   DTP_HIP(e);
   DTP_HIP(ef);
+  DTP_HIP(et);
   return DTP_OK;
 }
 
