@@ -134,6 +134,26 @@ def _counters(dirname, kernel_sub):
     return {k: sum(v) / len(v) for k, v in acc.items()}, (sum(durs) / len(durs) if durs else 0.0)
 
 
+def _timed_region(d: str):
+    """(launches, bench average ms, rocprofv3 average us) of the trace pass's timed region:
+    the bench's JSON line in the pass's log gives its launch count and HIP-event average,
+    which the last that many traced launches of the kernel are compared with."""
+    try:
+        line = [l for l in open(os.path.join(d, "trace.log")) if l.startswith("{")][-1]
+        roof = json.loads(line)["roofline"]
+        n, bench_ms = int(roof["launches"]), float(roof["avg_launch_ms"])
+        rows = [r for r in csv.DictReader(open(_one(os.path.join(d, "trace", "**", "*kernel_trace.csv"))))
+                if "affinity_bf16_kernel" in r["Kernel_Name"]]
+    except (OSError, ValueError, KeyError, IndexError, FileNotFoundError):
+        return None
+    rows.sort(key=lambda r: int(r["Start_Timestamp"]))
+    last = rows[-n:] if 0 < n <= len(rows) else []
+    if not last:
+        return None
+    traced = sum(int(r["End_Timestamp"]) - int(r["Start_Timestamp"]) for r in last) / len(last) / 1e3
+    return n, bench_ms, traced
+
+
 def summarize(d: str, profiles: str, workload: str, bench_cmd: str) -> None:
     stats = list(csv.DictReader(open(_one(os.path.join(d, "trace", "**", "*kernel_stats.csv")))))
     stats.sort(key=lambda r: -float(r["TotalDurationNs"]))
@@ -168,6 +188,13 @@ def summarize(d: str, profiles: str, workload: str, bench_cmd: str) -> None:
         a = aff[0]
         lines += ["", f"Affinity kernel: {a['Calls']} launches, average {float(a['AverageNs']) / 1e3:.1f} us, "
                   f"min {float(a['MinNs']) / 1e3:.1f} us, max {float(a['MaxNs']) / 1e3:.1f} us."]
+        timed = _timed_region(d)
+        if timed:
+            n, bench_ms, traced_us = timed
+            lines += ["", f"The traced bench run's timed region: {n} launches, average "
+                      f"{bench_ms * 1e3:.1f} us by the bench's HIP events on the launch stream, "
+                      f"{traced_us:.1f} us by rocprofv3 over the same (last {n}) launches; the "
+                      f"average above also counts the warm-up, serial and breakdown passes."]
     lines += ["", "## HBM traffic of the affinity kernel (--pmc FETCH_SIZE, WRITE_SIZE)", "",
               f"Counter scale from a plain {COPY_MIB} MiB device copy: FETCH_SIZE x{f_scale:.3f}, "
               f"WRITE_SIZE x{w_scale:.3f} (copy bytes / counter bytes).", "",
